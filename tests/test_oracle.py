@@ -1,0 +1,301 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle.
+
+Each test fixes the oracle to something independent of its own code: values
+derived by hand (tests/golden), a textbook/library routine (scipy, torch
+autograd), a closed form derived from Eq. (2), an invariant of the method, or
+central differences. A plausible slip anywhere in the oracle (a dropped term,
+a wrong sign or index, a transposed operand, a missing 1/tau) fails at least
+one of them.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.special as sps
+import torch
+
+from oracle import kd_topk_kl, teacher_distribution
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_cases.json")
+
+
+def _rand_case(N=6, D=5, V=13, K=4, seed=0, tau=1.0, ignore_frac=0.0, wscale=0.7):
+    rng = np.random.default_rng(seed)
+    h = rng.standard_normal((N, D))
+    W = rng.standard_normal((V, D)) * wscale
+    idx = np.stack([rng.choice(V, size=K, replace=False) for _ in range(N)])
+    tl = np.sort(rng.standard_normal((N, K)) * 3.0, axis=1)[:, ::-1].copy()
+    ign = None
+    if ignore_frac > 0:
+        ign = (rng.random(N) < ignore_frac).astype(np.uint8)
+        ign[0] = 0
+    return h, W, idx, tl, tau, ign
+
+
+# ---------------------------------------------------------------- golden ----
+def _golden_cases():
+    with open(GOLDEN) as f:
+        return json.load(f)["cases"]
+
+
+@pytest.mark.parametrize("case", _golden_cases(), ids=lambda c: c["name"])
+def test_hand_derived_cases(case):
+    ign = None if case["ignore"] is None else np.array(case["ignore"], dtype=np.uint8)
+    out = kd_topk_kl(np.array(case["h"]), np.array(case["W"]),
+                     np.array(case["teacher_idx"]), np.array(case["teacher_logit"]),
+                     tau=case["tau"], ignore=ign)
+    assert out["loss"] == pytest.approx(case["loss"], rel=1e-13, abs=1e-15)
+    np.testing.assert_allclose(out["loss_per_token"], case["loss_per_token"], rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(out["logZ"], case["logZ"], rtol=1e-13)
+    np.testing.assert_allclose(out["grad_hidden"], case["grad_hidden"], rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(out["grad_W"], case["grad_W"], rtol=1e-13, atol=1e-15)
+
+
+# --------------------------------------------------------- P1 Gibbs / Eq2 ---
+@pytest.mark.parametrize("tau", [1.0, 2.0])
+def test_p1_gibbs_decomposition(tau):
+    """With M = 1, Eq. (2) rearranges to l_t = KL(p || q_S / Q_S) - log Q_S with
+    Q_S = sum_{v in S} q_v; both terms are >= 0. Evaluated with scipy.rel_entr
+    and scipy.softmax, not with the oracle's formula."""
+    h, W, idx, tl, tau, _ = _rand_case(N=9, D=6, V=17, K=5, seed=1, tau=tau)
+    out = kd_topk_kl(h, W, idx, tl, tau=tau)
+    q = sps.softmax((h @ W.T) / tau, axis=1)
+    p = sps.softmax(tl / tau, axis=1)
+    for t in range(h.shape[0]):
+        qS = q[t, idx[t]]
+        QS = qS.sum()
+        expect = sps.rel_entr(p[t], qS / QS).sum() - np.log(QS)
+        assert out["loss_per_token"][t] == pytest.approx(expect, rel=1e-12)
+        assert out["loss_per_token"][t] >= 0.0
+    assert out["loss"] == pytest.approx(out["loss_per_token"].mean(), rel=1e-14)
+
+
+# ------------------------------------------------------------- P2 KL = 0 ----
+@pytest.mark.parametrize("tau", [1.0, 2.0])
+def test_p2_kl_zero_construction(tau):
+    """W = I_V makes hidden = logits. With z_t[idx_k] = teacher_logit_k and
+    z_t[v not in S_t] = -1e4, softmax_V(z/tau) restricted to S_t equals the
+    renormalised teacher and the outside mass underflows, so KL = 0."""
+    V, K, N = 24, 5, 4
+    h0, _, idx, tl, _, _ = _rand_case(N=N, D=3, V=V, K=K, seed=2)
+    h = np.full((N, V), -1e4)
+    for t in range(N):
+        h[t, idx[t]] = tl[t]
+    out = kd_topk_kl(h, np.eye(V), idx, tl, tau=tau)
+    assert abs(out["loss"]) < 1e-12
+    assert np.abs(out["loss_per_token"]).max() < 1e-12
+    assert np.abs(out["grad_hidden"]).max() < 1e-12
+
+
+# ----------------------------------------------------- P3 row-shift inv. ----
+def test_p3_row_shift_invariance():
+    """Adding c_t to every logit of row t changes nothing (Eq. 2: C and M log Z
+    both move by M c_t / tau). Realised with an extra hidden column equal to
+    c_t and a column of ones in W."""
+    h, W, idx, tl, tau, ign = _rand_case(N=7, D=5, V=19, K=4, seed=3, tau=1.5,
+                                          ignore_frac=0.3)
+    base = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign)
+    c = np.linspace(-40.0, 55.0, h.shape[0])
+    h2 = np.concatenate([h, c[:, None]], axis=1)
+    W2 = np.concatenate([W, np.ones((W.shape[0], 1))], axis=1)
+    out = kd_topk_kl(h2, W2, idx, tl, tau=tau, ignore=ign)
+    assert out["loss"] == pytest.approx(base["loss"], rel=1e-11)
+    np.testing.assert_allclose(out["grad_hidden"][:, :-1], base["grad_hidden"], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(out["grad_W"][:, :-1], base["grad_W"], rtol=1e-9, atol=1e-12)
+
+
+# ------------------------------------------------------- P4 K = V -----------
+@pytest.mark.parametrize("tau", [1.0, 2.0])
+def test_p4_full_vocab_is_textbook_kl(tau):
+    """With K = V the support is the whole vocabulary and l_t is the full
+    KL(p || q): compared with scipy.special.rel_entr and torch's kl_div."""
+    N, D, V = 5, 4, 11
+    rng = np.random.default_rng(4)
+    h = rng.standard_normal((N, D))
+    W = rng.standard_normal((V, D))
+    idx = np.stack([rng.permutation(V) for _ in range(N)])
+    tl = rng.standard_normal((N, V)) * 2.0
+    out = kd_topk_kl(h, W, idx, tl, tau=tau)
+    q = sps.softmax(h @ W.T / tau, axis=1)
+    for t in range(N):
+        pfull = np.zeros(V)
+        pfull[idx[t]] = sps.softmax(tl[t] / tau)
+        assert out["loss_per_token"][t] == pytest.approx(sps.rel_entr(pfull, q[t]).sum(), rel=1e-12)
+    z = torch.tensor(h @ W.T / tau)
+    P = torch.zeros(N, V, dtype=torch.float64)
+    P.scatter_(1, torch.tensor(idx), torch.softmax(torch.tensor(tl) / tau, dim=1))
+    kl = torch.nn.functional.kl_div(torch.log_softmax(z, dim=1), P, reduction="sum") / N
+    assert out["loss"] == pytest.approx(float(kl), rel=1e-12)
+
+
+# ------------------------------------------- P5 central differences ---------
+def test_p5_central_differences():
+    """Both gradients against central differences of the oracle's own loss,
+    tau = 2 and an ignore mask (N=5, D=8, V=33, K=4, chunk 2)."""
+    h, W, idx, tl, tau, _ = _rand_case(N=5, D=8, V=33, K=4, seed=5, tau=2.0)
+    ign = np.array([0, 1, 0, 0, 1], dtype=np.uint8)
+    out = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign, chunk=2)
+    eps = 1e-6
+
+    def L(hh, WW):
+        return kd_topk_kl(hh, WW, idx, tl, tau=tau, ignore=ign, chunk=2,
+                          want_grads=False)["loss"]
+
+    num_h = np.zeros_like(h)
+    for i in range(h.shape[0]):
+        for j in range(h.shape[1]):
+            hp = h.copy(); hp[i, j] += eps
+            hm = h.copy(); hm[i, j] -= eps
+            num_h[i, j] = (L(hp, W) - L(hm, W)) / (2 * eps)
+    num_W = np.zeros_like(W)
+    for i in range(W.shape[0]):
+        for j in range(W.shape[1]):
+            Wp = W.copy(); Wp[i, j] += eps
+            Wm = W.copy(); Wm[i, j] -= eps
+            num_W[i, j] = (L(h, Wp) - L(h, Wm)) / (2 * eps)
+    scale_h = np.abs(num_h).max()
+    scale_W = np.abs(num_W).max()
+    assert np.abs(out["grad_hidden"] - num_h).max() <= 1e-7 * scale_h
+    assert np.abs(out["grad_W"] - num_W).max() <= 1e-7 * scale_W
+    assert np.all(out["grad_hidden"][ign == 1] == 0.0)
+
+
+# ------------------------------------- textbook autograd (dense, torch) -----
+@pytest.mark.parametrize("tau", [1.0, 0.7, 2.0])
+def test_autograd_of_dense_textbook_loss(tau):
+    """Loss and both gradients against torch float64 autograd of the dense
+    textbook objective kl_div(log_softmax(h W^T / tau), P) / N_valid."""
+    h, W, idx, tl, _, ign = _rand_case(N=8, D=6, V=21, K=5, seed=6, tau=tau,
+                                        ignore_frac=0.3)
+    out = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign, chunk=3)
+    th = torch.tensor(h, requires_grad=True)
+    tW = torch.tensor(W, requires_grad=True)
+    valid = torch.tensor(ign == 0)
+    P = torch.zeros(h.shape[0], W.shape[0], dtype=torch.float64)
+    P.scatter_(1, torch.tensor(idx), torch.softmax(torch.tensor(tl) / tau, dim=1))
+    logq = torch.log_softmax(th @ tW.T / tau, dim=1)
+    per = torch.nn.functional.kl_div(logq, P, reduction="none").sum(dim=1)
+    loss = (per * valid).sum() / valid.sum()
+    loss.backward()
+    assert out["loss"] == pytest.approx(float(loss), rel=1e-12)
+    np.testing.assert_allclose(out["grad_hidden"], th.grad.numpy(), rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(out["grad_W"], tW.grad.numpy(), rtol=1e-10, atol=1e-14)
+
+
+# ------------------------------------------------------ P6 closed form dZ ---
+def test_p6_identity_head_gives_logit_gradient():
+    """With W = I_V the hidden gradient is the logit gradient itself, which
+    must equal torch autograd of log_softmax-based KL w.r.t. the logits."""
+    V, N, K, tau = 12, 3, 4, 2.0
+    rng = np.random.default_rng(7)
+    z = rng.standard_normal((N, V)) * 3
+    idx = np.stack([rng.choice(V, K, replace=False) for _ in range(N)])
+    tl = rng.standard_normal((N, K))
+    out = kd_topk_kl(z, np.eye(V), idx, tl, tau=tau)
+    tz = torch.tensor(z, requires_grad=True)
+    P = torch.zeros(N, V, dtype=torch.float64)
+    P.scatter_(1, torch.tensor(idx), torch.softmax(torch.tensor(tl) / tau, dim=1))
+    loss = torch.nn.functional.kl_div(torch.log_softmax(tz / tau, 1), P, reduction="sum") / N
+    loss.backward()
+    np.testing.assert_allclose(out["grad_hidden"], tz.grad.numpy(), rtol=1e-11, atol=1e-15)
+
+
+# ------------------------------------------------------ P7 zero sums --------
+def test_p7_zero_sum_of_logit_gradient():
+    """sum_v dL/dz_v = (M - M)/tau = 0 for every row, hence
+    sum_v grad_W[v, :] = 0; with W = I the rows of grad_hidden sum to 0."""
+    h, W, idx, tl, tau, ign = _rand_case(N=10, D=7, V=29, K=6, seed=8, tau=1.3,
+                                          ignore_frac=0.2)
+    out = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign)
+    assert np.abs(out["grad_W"].sum(axis=0)).max() < 1e-14 * max(1, np.abs(out["grad_W"]).max()) * 100
+    V = 29
+    out2 = kd_topk_kl(h @ W.T, np.eye(V), idx, tl, tau=tau, ignore=ign)
+    assert np.abs(out2["grad_hidden"].sum(axis=1)).max() < 1e-15 * 100
+
+
+# --------------------------------------------------- P8 chunk invariance ----
+@pytest.mark.parametrize("chunk", [1, 7, 64, 50, 55])
+def test_p8_chunk_invariance(chunk):
+    h, W, idx, tl, tau, ign = _rand_case(N=50, D=6, V=31, K=5, seed=9, tau=1.0,
+                                          ignore_frac=0.1)
+    ref = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign, chunk=None)
+    out = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign, chunk=chunk)
+    assert out["loss"] == pytest.approx(ref["loss"], rel=1e-13)
+    np.testing.assert_allclose(out["grad_hidden"], ref["grad_hidden"], rtol=1e-12, atol=1e-16)
+    np.testing.assert_allclose(out["grad_W"], ref["grad_W"], rtol=1e-12, atol=1e-16)
+
+
+# ------------------------------------------------- P9 ignore = delete -------
+def test_p9_ignore_equals_delete():
+    h, W, idx, tl, tau, _ = _rand_case(N=9, D=5, V=23, K=4, seed=10, tau=1.0)
+    ign = np.zeros(9, dtype=np.uint8)
+    ign[[2, 5]] = 1
+    keep = ign == 0
+    a = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign)
+    b = kd_topk_kl(h[keep], W, idx[keep], tl[keep], tau=tau)
+    assert a["loss"] == pytest.approx(b["loss"], rel=1e-14)
+    np.testing.assert_allclose(a["grad_hidden"][keep], b["grad_hidden"], rtol=1e-14, atol=1e-17)
+    assert np.all(a["grad_hidden"][~keep] == 0.0)
+    assert np.all(a["loss_per_token"][~keep] == 0.0)
+    np.testing.assert_allclose(a["grad_W"], b["grad_W"], rtol=1e-12, atol=1e-17)
+
+
+def test_all_ignored_gives_zero():
+    h, W, idx, tl, tau, _ = _rand_case(N=4, D=5, V=11, K=3, seed=11)
+    out = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=np.ones(4, dtype=np.uint8))
+    assert out["loss"] == 0.0
+    assert np.all(out["grad_hidden"] == 0.0) and np.all(out["grad_W"] == 0.0)
+
+
+# ---------------------------------------------- P10 batch duplication -------
+def test_p10_batch_duplication():
+    h, W, idx, tl, tau, ign = _rand_case(N=6, D=4, V=15, K=3, seed=12, tau=1.7,
+                                          ignore_frac=0.2)
+    a = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign)
+    dup = lambda x: None if x is None else np.concatenate([x, x], axis=0)
+    b = kd_topk_kl(dup(h), W, dup(idx), dup(tl), tau=tau, ignore=dup(ign))
+    assert b["loss"] == pytest.approx(a["loss"], rel=1e-14)
+    np.testing.assert_allclose(b["grad_W"], a["grad_W"], rtol=1e-12, atol=1e-17)
+    np.testing.assert_allclose(b["grad_hidden"][:6], a["grad_hidden"] / 2, rtol=1e-14, atol=1e-17)
+
+
+# --------------------------------------------- mean denominator override ----
+def test_subset_rows_with_batch_denominator():
+    """Rows are independent given the batch's N_valid: evaluating a subset of
+    rows with the full batch's denominator reproduces those rows exactly."""
+    h, W, idx, tl, tau, ign = _rand_case(N=12, D=5, V=17, K=4, seed=13,
+                                          ignore_frac=0.25)
+    full = kd_topk_kl(h, W, idx, tl, tau=tau, ignore=ign)
+    rows = np.array([1, 4, 7, 11])
+    nv = int((ign == 0).sum())
+    sub = kd_topk_kl(h[rows], W, idx[rows], tl[rows], tau=tau, ignore=ign[rows],
+                     mean_denominator=nv)
+    np.testing.assert_allclose(sub["loss_per_token"], full["loss_per_token"][rows], rtol=1e-14)
+    np.testing.assert_allclose(sub["grad_hidden"], full["grad_hidden"][rows], rtol=1e-13, atol=1e-18)
+
+
+# ----------------------------------------------------- teacher softmax ------
+def test_teacher_distribution_matches_scipy():
+    rng = np.random.default_rng(14)
+    tl = rng.standard_normal((7, 9)) * 5
+    for tau in (1.0, 2.0, 0.5):
+        np.testing.assert_allclose(teacher_distribution(tl, tau),
+                                   sps.softmax(tl / tau, axis=1), rtol=1e-14)
+
+
+# ------------------------------------------------ statistical sanity --------
+def test_random_init_expected_loss():
+    """Not a pin: at random init E[l] ~ log V + sigma_z^2/(2 tau^2) + sum p log p
+    (second-order expansion of log Z with logits of variance sigma_z^2)."""
+    N, D, V, K, tau = 64, 256, 4096, 16, 1.0
+    rng = np.random.default_rng(15)
+    h = rng.standard_normal((N, D))
+    W = rng.standard_normal((V, D)) * 0.02
+    idx = np.stack([rng.choice(V, K, replace=False) for _ in range(N)])
+    tl = np.sort(rng.standard_normal((N, K)) * 3, axis=1)[:, ::-1]
+    out = kd_topk_kl(h, W, idx, tl, tau=tau, want_grads=False)
+    p = sps.softmax(tl / tau, axis=1)
+    negent = (p * np.log(p)).sum(axis=1).mean()
+    expect = np.log(V) + D * 0.02 ** 2 / (2 * tau ** 2) + negent
+    assert abs(out["loss"] - expect) < 0.15
