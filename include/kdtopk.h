@@ -1,0 +1,153 @@
+/*
+ * kdtopk.h - C ABI of the fused, chunked top-K KL distillation loss for
+ * AMD MI355X (gfx950).
+ *
+ * The operation is the "full chunked KL computation" of §3.2.3 and
+ * Algorithm 1 of "Efficient Knowledge Distillation for LLMs: Offline Top-K
+ * Logits and a Fused Chunked KL Loss": the student output projection
+ * z = h W^T is fused into a forward KL against a cached top-K teacher, the
+ * rows are processed in chunks of C_s tokens, and the [N, V] logit tensor is
+ * never stored. Per token t (Eq. 1 and its decomposition Eq. 2 in §3.2):
+ *
+ *     l_t = sum_{k} p_tk log p_tk  -  sum_{k} p_tk y_t[idx_tk]  +  M_t log Z_t
+ *
+ * with y_t = z_t / tau, log Z_t = logsumexp_v y_tv, p_t = softmax over the K
+ * cached entries of teacher_logit_t / tau and M_t = sum_k p_tk. The loss is the
+ * mean of l_t over non-ignored tokens (§3, after Eq. 1). Gradients use the
+ * closed form of Eq. (3) (§3.2.3): dL/dz_tv = g_t / tau (M_t q_tv - p_tv) with
+ * q_t = softmax(y_t) and g_t = 1/N_valid for non-ignored tokens, 0 otherwise;
+ * grad_hidden = G W and grad_W (+)= G^T h, as in Algorithm 1's backward.
+ *
+ * Conventions for every entry point:
+ *   - All tensor pointers are DEVICE pointers, row-major, densely packed.
+ *   - The caller allocates and owns every buffer, including the workspace.
+ *     The library never allocates, frees, or keeps a pointer after return.
+ *   - Work is enqueued asynchronously on `hip_stream` (a hipStream_t passed as
+ *     void*, NULL = the default stream). kd_topk_kl_fwd_bwd never
+ *     synchronises: read `loss` after synchronising the stream.
+ *   - Every argument is checked on the host before anything is enqueued. On
+ *     any error nothing is launched, no output is touched, and the function
+ *     returns the error code.
+ *   - Results are deterministic: identical inputs and chunk size give
+ *     bitwise identical outputs (no floating-point atomics).
+ *   - Calls are reentrant; concurrent calls need distinct workspaces.
+ */
+#ifndef KDTOPK_H
+#define KDTOPK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KDTOPK_ABI_VERSION 1
+
+typedef enum kd_status {
+  KD_OK = 0,
+  KD_ERR_NULL_PTR = 1,           /* a required pointer is NULL */
+  KD_ERR_BAD_SHAPE = 2,          /* N < 0, D/V/K <= 0, K > V, or a size limit */
+  KD_ERR_BAD_ARG = 3,            /* chunk <= 0, tau not finite or <= 0, flags */
+  KD_ERR_UNSUPPORTED = 4,        /* dtype, D % 64 != 0, misaligned pointer */
+  KD_ERR_WORKSPACE_TOO_SMALL = 5,
+  KD_ERR_BAD_INDEX = 6,          /* a teacher index outside [0, V) or repeated */
+  KD_ERR_DEVICE = 7              /* a HIP launch or runtime error */
+} kd_status;
+
+typedef enum kd_dtype {
+  KD_F32 = 0,                    /* fp32 inputs, fp32 arithmetic throughout */
+  KD_BF16 = 1                    /* bf16 inputs, bf16 MFMA, fp32 accumulate */
+} kd_dtype;
+
+/* Problem description (Algorithm 1's inputs: h, W, the support and C_s). */
+typedef struct kd_problem {
+  int64_t N;           /* tokens = rows of hidden; 0 <= N < 2^31            */
+  int64_t D;           /* hidden size d; 64 <= D <= 65536, D % 64 == 0       */
+  int64_t V;           /* vocabulary size; 1 <= V <= 4194304                 */
+  int64_t chunk;       /* rows per chunk C_s; >= 1 (min(chunk, N) is used)   */
+  int32_t K;           /* cached teacher entries per token; 1 <= K <= V      */
+  int32_t dtype;       /* kd_dtype of hidden, W and grad_hidden              */
+  float temperature;   /* tau; finite and > 0                                */
+  int32_t flags;       /* reserved; must be 0                                */
+} kd_problem;
+
+/*
+ * Bytes of device workspace kd_topk_kl_fwd_bwd and kd_topk_kl_check_indices
+ * need for problem *p. Pure host function: touches no device. The size is
+ * O(N/256 + C_s (V + D + K) + V D): it grows with N only through a per-256-row
+ * array of loss partials, never as N*V.
+ * Errors: KD_ERR_NULL_PTR if p or bytes is NULL; the shape/argument errors of
+ * kd_topk_kl_fwd_bwd otherwise.
+ */
+kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
+
+/*
+ * Fused chunked top-K KL forward + backward (§3.2.3, Algorithm 1, Eqs. 1-3).
+ *
+ *   hidden        [N, D] dtype        student hidden states h (row t = token t)
+ *   W             [V, D] dtype        output projection
+ *   teacher_idx   [N, K] int32        support S_t: K distinct indices in [0, V)
+ *                                     per row (not range-checked here; see
+ *                                     kd_topk_kl_check_indices)
+ *   teacher_logit [N, K] fp32         teacher logits of the support; the
+ *                                     teacher distribution is their softmax
+ *                                     over the K entries at temperature tau
+ *   ignore        [N] uint8 or NULL   nonzero = token excluded from the loss
+ *                                     and from the mean's count; NULL = none
+ *   loss          [1] fp32            out: mean of l_t over non-ignored
+ *                                     tokens (0 if there are none)
+ *   loss_per_token [N] fp32 or NULL   out: l_t (0 on ignored tokens)
+ *   grad_hidden   [N, D] dtype or NULL  out: dL/dh; NULL skips its GEMMs
+ *   grad_W        [V, D] fp32 or NULL   out: dL/dW; NULL skips its GEMMs
+ *   accumulate_grad_W  0: grad_W = dL/dW;  1: grad_W += dL/dW (micro-batch
+ *                                     accumulation)
+ *   workspace, workspace_bytes        device scratch of at least
+ *                                     kd_topk_kl_workspace_size bytes,
+ *                                     16-byte aligned
+ *   hip_stream                        hipStream_t or NULL
+ *
+ * Pointers hidden, W, grad_hidden, grad_W and workspace must be 16-byte
+ * aligned (KD_ERR_UNSUPPORTED otherwise). hidden, W, teacher_idx,
+ * teacher_logit and loss are required (KD_ERR_NULL_PTR); with N == 0 only
+ * loss (and grad_W when given) are written. Launch failures return
+ * KD_ERR_DEVICE; work enqueued before the failure may have run.
+ */
+kd_status kd_topk_kl_fwd_bwd(const kd_problem* p,
+                             const void* hidden,
+                             const void* W,
+                             const int32_t* teacher_idx,
+                             const float* teacher_logit,
+                             const uint8_t* ignore,
+                             float* loss,
+                             float* loss_per_token,
+                             void* grad_hidden,
+                             float* grad_W,
+                             int accumulate_grad_W,
+                             void* workspace,
+                             size_t workspace_bytes,
+                             void* hip_stream);
+
+/*
+ * Checks that every teacher index lies in [0, V) and that no row repeats an
+ * index (the support S_t of §3.2 is a set). Synchronises `hip_stream`.
+ * Returns KD_OK, KD_ERR_BAD_INDEX, or an argument/device error. Uses the
+ * first bytes of `workspace` (same size rule as kd_topk_kl_fwd_bwd).
+ */
+kd_status kd_topk_kl_check_indices(const kd_problem* p,
+                                   const int32_t* teacher_idx,
+                                   void* workspace,
+                                   size_t workspace_bytes,
+                                   void* hip_stream);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* kd_status_string(int status);
+
+/* KDTOPK_ABI_VERSION of the loaded library. */
+int kd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KDTOPK_H */

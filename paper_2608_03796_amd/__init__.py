@@ -1,0 +1,188 @@
+"""Fused chunked top-K KL distillation loss on AMD MI355X (gfx950).
+
+Python binding of libkdtopk.so (C ABI in include/kdtopk.h). The binding only
+marshals arguments: PyTorch provides device memory and the current stream;
+every step of the loss runs in the library's HIP kernels. There is no CPU or
+PyTorch fallback: if the library is missing, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkdtopk.so")
+
+KD_F32 = 0
+KD_BF16 = 1
+
+STATUS = {
+    0: "KD_OK", 1: "KD_ERR_NULL_PTR", 2: "KD_ERR_BAD_SHAPE", 3: "KD_ERR_BAD_ARG",
+    4: "KD_ERR_UNSUPPORTED", 5: "KD_ERR_WORKSPACE_TOO_SMALL", 6: "KD_ERR_BAD_INDEX",
+    7: "KD_ERR_DEVICE",
+}
+EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_check_indices",
+            "kd_status_string", "kd_abi_version")
+
+
+class KdError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {STATUS.get(code, code)}")
+
+
+class KdProblem(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("D", ctypes.c_int64), ("V", ctypes.c_int64),
+                ("chunk", ctypes.c_int64), ("K", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("temperature", ctypes.c_float), ("flags", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Loads libkdtopk.so (built by paper_2608_03796_amd.build). Raises if absent."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is not built; run `python -m paper_2608_03796_amd.build`")
+    lib = ctypes.CDLL(p)
+    vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    lib.kd_topk_kl_workspace_size.argtypes = [ctypes.POINTER(KdProblem), ctypes.POINTER(sz)]
+    lib.kd_topk_kl_workspace_size.restype = ctypes.c_int
+    lib.kd_topk_kl_fwd_bwd.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp, vp, vp, vp,
+                                       vp, ctypes.c_int, vp, sz, vp]
+    lib.kd_topk_kl_fwd_bwd.restype = ctypes.c_int
+    lib.kd_topk_kl_check_indices.argtypes = [ctypes.POINTER(KdProblem), vp, vp, sz, vp]
+    lib.kd_topk_kl_check_indices.restype = ctypes.c_int
+    lib.kd_status_string.argtypes = [ctypes.c_int]
+    lib.kd_status_string.restype = ctypes.c_char_p
+    lib.kd_abi_version.argtypes = []
+    lib.kd_abi_version.restype = ctypes.c_int
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def problem(N, D, V, K, chunk, tau, dtype, flags=0) -> KdProblem:
+    return KdProblem(int(N), int(D), int(V), int(chunk), int(K), int(dtype), float(tau), int(flags))
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t == torch.bfloat16:
+        return KD_BF16
+    if t == torch.float32:
+        return KD_F32
+    raise TypeError(f"unsupported dtype {t}")
+
+
+def workspace_size(N, D, V, K, chunk, tau=1.0, dtype=KD_BF16) -> int:
+    lib = load_library()
+    pr = problem(N, D, V, K, chunk, tau, dtype)
+    out = ctypes.c_size_t(0)
+    rc = lib.kd_topk_kl_workspace_size(ctypes.byref(pr), ctypes.byref(out))
+    if rc != 0:
+        raise KdError(rc, "kd_topk_kl_workspace_size")
+    return int(out.value)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(device):
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def alloc_workspace(N, D, V, K, chunk, tau, dtype, device):
+    import torch
+    n = workspace_size(N, D, V, K, chunk, tau, dtype)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
+            chunk: int = 4096, grad_hidden: bool = True, grad_W: bool = True,
+            loss_per_token: bool = False, grad_W_out=None, accumulate_grad_W: bool = False,
+            workspace=None, out=None):
+    """One call of kd_topk_kl_fwd_bwd on the current stream.
+
+    hidden [N, D] and W [V, D] (bf16 or fp32, same dtype), teacher_idx [N, K]
+    int32, teacher_logit [N, K] fp32, ignore [N] uint8 or None. Returns a dict
+    with 'loss' (0-d fp32 tensor), and 'loss_per_token', 'grad_hidden',
+    'grad_W' when requested. `out` may carry preallocated output tensors
+    (keys as returned) to make repeated calls allocation-free.
+    """
+    import torch
+    lib = load_library()
+    if hidden.device.type != "cuda":
+        raise ValueError("tensors must be on a GPU")
+    N, D = hidden.shape
+    V = W.shape[0]
+    K = teacher_idx.shape[1] if teacher_idx.dim() == 2 else 0
+    dt = _dtype_code(hidden.dtype)
+    if W.dtype != hidden.dtype:
+        raise TypeError("hidden and W must share a dtype")
+    for name, t, want in (("teacher_idx", teacher_idx, torch.int32),
+                          ("teacher_logit", teacher_logit, torch.float32)):
+        if t.dtype != want:
+            raise TypeError(f"{name} must be {want}")
+    if ignore is not None and ignore.dtype != torch.uint8:
+        raise TypeError("ignore must be uint8")
+    tensors = [hidden, W, teacher_idx, teacher_logit] + ([ignore] if ignore is not None else [])
+    for t in tensors:
+        if not t.is_contiguous():
+            raise ValueError("inputs must be contiguous")
+    out = dict(out or {})
+    dev = hidden.device
+    if "loss" not in out:
+        out["loss"] = torch.empty((), dtype=torch.float32, device=dev)
+    if loss_per_token and "loss_per_token" not in out:
+        out["loss_per_token"] = torch.empty(N, dtype=torch.float32, device=dev)
+    if grad_hidden and "grad_hidden" not in out:
+        out["grad_hidden"] = torch.empty(N, D, dtype=hidden.dtype, device=dev)
+    if grad_W:
+        if grad_W_out is not None:
+            out["grad_W"] = grad_W_out
+        elif "grad_W" not in out:
+            out["grad_W"] = torch.empty(V, D, dtype=torch.float32, device=dev)
+    pr = problem(N, D, V, K, chunk, tau, dt)
+    if workspace is None:
+        workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
+    rc = lib.kd_topk_kl_fwd_bwd(
+        ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+        _ptr(ignore), _ptr(out["loss"]), _ptr(out.get("loss_per_token") if loss_per_token else None),
+        _ptr(out.get("grad_hidden") if grad_hidden else None),
+        _ptr(out.get("grad_W") if grad_W else None), int(bool(accumulate_grad_W)),
+        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
+    if rc != 0:
+        raise KdError(rc, "kd_topk_kl_fwd_bwd")
+    res = {"loss": out["loss"]}
+    if loss_per_token:
+        res["loss_per_token"] = out["loss_per_token"]
+    if grad_hidden:
+        res["grad_hidden"] = out["grad_hidden"]
+    if grad_W:
+        res["grad_W"] = out["grad_W"]
+    return res
+
+
+def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, workspace=None):
+    """True if every index is in [0, V) and no row repeats one (synchronises)."""
+    lib = load_library()
+    N, K = teacher_idx.shape
+    pr = problem(N, D, V, K, chunk, tau, dtype)
+    if workspace is None:
+        workspace = alloc_workspace(N, D, V, K, chunk, tau, dtype, teacher_idx.device)
+    rc = lib.kd_topk_kl_check_indices(ctypes.byref(pr), _ptr(teacher_idx), _ptr(workspace),
+                                      ctypes.c_size_t(workspace.numel()),
+                                      _stream_handle(teacher_idx.device))
+    if rc == 6:
+        return False
+    if rc != 0:
+        raise KdError(rc, "kd_topk_kl_check_indices")
+    return True

@@ -1,0 +1,242 @@
+// C ABI of the fused chunked top-K KL loss: argument checks, workspace plan
+// and the chunk schedule of Algorithm 1 (§3.2.3). Plain C++: every device
+// operation goes through the launchers of kd_kernels.hip.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/kdtopk.h"
+#include "kd_launch.h"
+
+namespace {
+
+constexpr int64_t kTile = 256;
+constexpr int64_t kMaxN = (int64_t)1 << 31;     // N < 2^31
+constexpr int64_t kMaxV = (int64_t)1 << 20;     // keeps 32-bit buffer offsets in range
+constexpr int64_t kMaxD = 65536;
+constexpr int64_t kMaxChunk = (int64_t)1 << 20; // rows per chunk actually used
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t rup(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Plan {
+  int64_t N, D, V, K;
+  int eb;              // element bytes of hidden / W / dZ
+  int64_t c;           // rows per chunk
+  int64_t cp;          // c rounded up to the 256-row tile
+  int64_t Vp;          // V rounded up to the 256-column tile
+  int64_t nVT;         // vocabulary tiles
+  int64_t nchunks;
+  int64_t nblk;        // loss partials of a full chunk
+  int dh_split;
+  size_t off_misc, off_p, off_rows, off_pm, off_ps, off_pc, off_lossp, off_dz, off_dzt, off_wt,
+      off_hct, off_dhs, total;
+};
+
+kd_status check_problem(const kd_problem* p) {
+  if (p == nullptr) return KD_ERR_NULL_PTR;
+  if (p->flags != 0) return KD_ERR_BAD_ARG;
+  if (p->dtype != KD_F32 && p->dtype != KD_BF16) return KD_ERR_UNSUPPORTED;
+  if (p->N < 0 || p->N >= kMaxN) return KD_ERR_BAD_SHAPE;
+  if (p->D < 64 || p->D > kMaxD) return KD_ERR_BAD_SHAPE;
+  if (p->V < 1 || p->V > kMaxV) return KD_ERR_BAD_SHAPE;
+  if (p->K < 1 || (int64_t)p->K > p->V) return KD_ERR_BAD_SHAPE;
+  if (p->chunk < 1) return KD_ERR_BAD_ARG;
+  if (!(isfinite(p->temperature) && p->temperature > 0.0f)) return KD_ERR_BAD_ARG;
+  if (p->D % 64 != 0) return KD_ERR_UNSUPPORTED;
+  return KD_OK;
+}
+
+// Split of the dH GEMM's K range (the vocabulary) so that the number of
+// workgroups fills whole waves of the 256 compute units.
+int choose_dh_split(int64_t tiles, int64_t ksteps) {
+  int best = 1;
+  double best_eff = (double)tiles / (double)(cdiv(tiles, 256) * 256);
+  for (int s = 2; s <= 16; ++s) {
+    if (ksteps / s < 8) break;
+    const double eff = (double)(tiles * s) / (double)(cdiv(tiles * s, 256) * 256);
+    if (eff > best_eff + 0.05) {
+      best = s;
+      best_eff = eff;
+    }
+  }
+  return best;
+}
+
+Plan make_plan(const kd_problem* p) {
+  Plan pl{};
+  pl.N = p->N;
+  pl.D = p->D;
+  pl.V = p->V;
+  pl.K = p->K;
+  pl.eb = p->dtype == KD_BF16 ? 2 : 4;
+  pl.c = std::min<int64_t>(std::min<int64_t>(p->chunk, std::max<int64_t>(p->N, 1)), kMaxChunk);
+  pl.cp = rup(pl.c, kTile);
+  pl.Vp = rup(pl.V, kTile);
+  pl.nVT = pl.Vp / kTile;
+  pl.nchunks = cdiv(pl.N, pl.c);
+  pl.nblk = cdiv(pl.c, kTile);
+  const int64_t dh_tiles = cdiv(pl.c, kTile) * cdiv(pl.D, kTile);
+  pl.dh_split = choose_dh_split(dh_tiles, pl.Vp * pl.eb / 128);
+  size_t t = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = align256(t);
+    t = o + bytes;
+    return o;
+  };
+  pl.off_misc = take(256);
+  pl.off_p = take((size_t)pl.cp * pl.K * 4);
+  pl.off_rows = take((size_t)6 * pl.cp * 4);
+  pl.off_pm = take((size_t)pl.cp * pl.nVT * 4);
+  pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
+  pl.off_pc = take((size_t)pl.cp * pl.nVT * 4);
+  pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
+  pl.off_dz = take((size_t)pl.cp * pl.Vp * pl.eb);
+  pl.off_dzt = take((size_t)pl.Vp * pl.cp * pl.eb);
+  pl.off_wt = take((size_t)pl.D * pl.Vp * pl.eb);
+  pl.off_hct = take((size_t)pl.D * pl.cp * pl.eb);
+  pl.off_dhs = pl.dh_split > 1 ? take((size_t)pl.dh_split * pl.c * pl.D * 4) : 0;
+  pl.total = align256(t);
+  return pl;
+}
+
+inline bool aligned16(const void* q) { return ((uintptr_t)q & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int kd_abi_version(void) { return KDTOPK_ABI_VERSION; }
+
+const char* kd_status_string(int s) {
+  switch (s) {
+    case KD_OK: return "KD_OK: success";
+    case KD_ERR_NULL_PTR: return "KD_ERR_NULL_PTR: a required pointer is NULL";
+    case KD_ERR_BAD_SHAPE: return "KD_ERR_BAD_SHAPE: invalid N, D, V or K, or a size limit";
+    case KD_ERR_BAD_ARG: return "KD_ERR_BAD_ARG: invalid chunk, temperature, flags or mode";
+    case KD_ERR_UNSUPPORTED: return "KD_ERR_UNSUPPORTED: dtype, D % 64 != 0 or misaligned pointer";
+    case KD_ERR_WORKSPACE_TOO_SMALL: return "KD_ERR_WORKSPACE_TOO_SMALL: workspace below the required size";
+    case KD_ERR_BAD_INDEX: return "KD_ERR_BAD_INDEX: teacher index outside [0, V) or repeated in a row";
+    case KD_ERR_DEVICE: return "KD_ERR_DEVICE: HIP launch or runtime error";
+    default: return "unknown kd_status";
+  }
+}
+
+kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes) {
+  if (p == nullptr || bytes == nullptr) return KD_ERR_NULL_PTR;
+  const kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  *bytes = make_plan(p).total;
+  return KD_OK;
+}
+
+kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void* W,
+                             const int32_t* teacher_idx, const float* teacher_logit,
+                             const uint8_t* ignore, float* loss, float* loss_per_token,
+                             void* grad_hidden, float* grad_W, int accumulate_grad_W,
+                             void* workspace, size_t workspace_bytes, void* hip_stream) {
+  kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  if (loss == nullptr || workspace == nullptr) return KD_ERR_NULL_PTR;
+  if (p->N > 0 && (hidden == nullptr || W == nullptr || teacher_idx == nullptr ||
+                   teacher_logit == nullptr))
+    return KD_ERR_NULL_PTR;
+  if (accumulate_grad_W != 0 && accumulate_grad_W != 1) return KD_ERR_BAD_ARG;
+  if (!aligned16(hidden) || !aligned16(W) || !aligned16(grad_hidden) || !aligned16(grad_W) ||
+      !aligned16(workspace))
+    return KD_ERR_UNSUPPORTED;
+  const Plan pl = make_plan(p);
+  if (workspace_bytes < pl.total) return KD_ERR_WORKSPACE_TOO_SMALL;
+
+  char* ws = static_cast<char*>(workspace);
+  int* nvalid = reinterpret_cast<int*>(ws + pl.off_misc);
+  float* inv_nvalid = reinterpret_cast<float*>(ws + pl.off_misc + 4);
+  float* lossp = reinterpret_cast<float*>(ws + pl.off_lossp);
+  const bool want_dh = grad_hidden != nullptr && pl.N > 0;
+  const bool want_dw = grad_W != nullptr && pl.N > 0;
+
+  KdPrepareArgs pa{};
+  pa.dtype = p->dtype;
+  pa.N = pl.N;
+  pa.D = pl.D;
+  pa.V = pl.V;
+  pa.ignore = ignore;
+  pa.nvalid = nvalid;
+  pa.inv_nvalid = inv_nvalid;
+  pa.W = W;
+  pa.Wt = want_dh ? ws + pl.off_wt : nullptr;
+  pa.ldw = pl.Vp;
+  pa.zero_gW = (grad_W != nullptr && pl.N == 0 && !accumulate_grad_W) ? grad_W : nullptr;
+  if (kd_launch_prepare(&pa, hip_stream) != 0) return KD_ERR_DEVICE;
+
+  float* rows = reinterpret_cast<float*>(ws + pl.off_rows);
+  int64_t n_partials = 0;
+  for (int64_t ci = 0; ci < pl.nchunks; ++ci) {
+    const int64_t row0 = ci * pl.c;
+    const int rcount = (int)std::min<int64_t>(pl.c, pl.N - row0);
+    KdChunkArgs a{};
+    a.dtype = p->dtype;
+    a.D = pl.D;
+    a.V = pl.V;
+    a.K = (int)pl.K;
+    a.row0 = row0;
+    a.rows = rcount;
+    a.inv_tau = 1.0f / p->temperature;
+    a.W = W;
+    a.Hc = static_cast<const char*>(hidden) + row0 * pl.D * pl.eb;
+    a.tidx = teacher_idx + row0 * pl.K;
+    a.tlogit = teacher_logit;
+    a.ignore = ignore;
+    a.inv_nvalid = inv_nvalid;
+    a.p = reinterpret_cast<float*>(ws + pl.off_p);
+    a.rowM = rows;
+    a.rowH = rows + pl.cp;
+    a.rowCoef = rows + 2 * pl.cp;
+    a.rowCoefM = rows + 3 * pl.cp;
+    a.rowL2 = rows + 4 * pl.cp;
+    a.part_m = reinterpret_cast<float*>(ws + pl.off_pm);
+    a.part_s = reinterpret_cast<float*>(ws + pl.off_ps);
+    a.part_C = reinterpret_cast<float*>(ws + pl.off_pc);
+    a.nVT = (int)pl.nVT;
+    a.dZ = want_dh ? ws + pl.off_dz : nullptr;
+    a.ldz = pl.Vp;
+    a.dZt = want_dw ? ws + pl.off_dzt : nullptr;
+    a.ldzt = pl.cp;
+    a.Hct = want_dw ? ws + pl.off_hct : nullptr;
+    a.ldh = pl.cp;
+    a.Wt = ws + pl.off_wt;
+    a.ldw = pl.Vp;
+    a.dh_split = pl.dh_split;
+    a.dh_partial = pl.dh_split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
+    a.loss_per_token = loss_per_token ? loss_per_token + row0 : nullptr;
+    a.block_partial = lossp + n_partials;
+    a.gH = want_dh ? static_cast<char*>(grad_hidden) + row0 * pl.D * pl.eb : nullptr;
+    a.gW = want_dw ? grad_W : nullptr;
+    a.dw_beta = (ci > 0 || accumulate_grad_W) ? 1 : 0;
+    if (kd_launch_chunk(&a, hip_stream) != 0) return KD_ERR_DEVICE;
+    n_partials += cdiv(rcount, kTile);
+  }
+  if (kd_launch_finalize(lossp, (int)n_partials, inv_nvalid, loss, hip_stream) != 0)
+    return KD_ERR_DEVICE;
+  return KD_OK;
+}
+
+kd_status kd_topk_kl_check_indices(const kd_problem* p, const int32_t* teacher_idx,
+                                   void* workspace, size_t workspace_bytes, void* hip_stream) {
+  kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  if (workspace == nullptr || (p->N > 0 && teacher_idx == nullptr)) return KD_ERR_NULL_PTR;
+  if (!aligned16(workspace)) return KD_ERR_UNSUPPORTED;
+  const Plan pl = make_plan(p);
+  if (workspace_bytes < pl.total) return KD_ERR_WORKSPACE_TOO_SMALL;
+  int* flag = reinterpret_cast<int*>(static_cast<char*>(workspace) + pl.off_misc + 8);
+  int host_flag = 0;
+  if (kd_launch_check_indices(teacher_idx, p->N, p->K, p->V, flag, &host_flag, hip_stream) != 0)
+    return KD_ERR_DEVICE;
+  return host_flag ? KD_ERR_BAD_INDEX : KD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,587 @@
+// HIP kernels (gfx950) of the fused chunked top-K KL loss and their launchers.
+//
+// Per call:    count_valid, [W^T copy]
+// Per chunk:   teacher_prologue  -> p, M, H, g/tau                 (§3.2, Eq. 2 terms)
+//              logits_lse        -> per (token, vocab tile) max / sum-exp partials
+//              lse_merge         -> log Z per token                 (Alg. 1 normaliser)
+//              dz                -> recomputed logits, dZ = g/tau (M q - p) in LDS,
+//                                   stored as dZ[c, V] and dZ^T[V, c]; C partials
+//              row_loss          -> l_t = H - C/tau + M log Z       (Eq. 2)
+//              [H_c^T copy], dh (+ split reduce), dw (fp32 accumulate)
+// Per call:    finalize_loss     -> mean over non-ignored tokens
+#include "kd_device.h"
+#include "kd_launch.h"
+
+namespace kd {
+
+// ------------------------------------------------------------------ small --
+__global__ void k_count_valid(const uint8_t* ignore, int64_t N, int* nvalid, float* inv_nvalid) {
+  __shared__ int red[256];
+  int c = 0;
+  for (int64_t i = threadIdx.x; i < N; i += 256) c += (ignore == nullptr || ignore[i] == 0) ? 1 : 0;
+  red[threadIdx.x] = c;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    nvalid[0] = red[0];
+    inv_nvalid[0] = red[0] > 0 ? 1.0f / (float)red[0] : 0.0f;
+  }
+}
+
+__global__ void k_fill_f32(float* p, int64_t n, float v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) p[i] = v;
+}
+
+// Teacher distribution over the K cached entries of each chunk row (§3.2):
+// p = softmax(teacher_logit / tau), M = sum p, H = sum p log p (0 log 0 = 0),
+// coef = g/tau with g = 1/N_valid (0 for ignored rows). One wave per row.
+__global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, int64_t row0,
+                                   int rows, int K, float inv_tau, const float* inv_nvalid,
+                                   float* p_out, float* rowM, float* rowH, float* rowCoef,
+                                   float* rowCoefM) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int64_t t = row0 + r;
+  const float* u = tlogit + t * (int64_t)K;
+  float mx = -INFINITY;
+  for (int k = lane; k < K; k += 64) mx = fmaxf(mx, u[k] * inv_tau);
+  mx = wave_max(mx);
+  float s = 0.f;
+  for (int k = lane; k < K; k += 64) s += expf(u[k] * inv_tau - mx);
+  s = wave_sum(s);
+  const float logs = logf(s);
+  float m = 0.f, h = 0.f;
+  for (int k = lane; k < K; k += 64) {
+    const float lp = u[k] * inv_tau - mx - logs;
+    const float pk = expf(lp);
+    p_out[(int64_t)r * K + k] = pk;
+    m += pk;
+    h += pk > 0.f ? pk * lp : 0.f;
+  }
+  m = wave_sum(m);
+  h = wave_sum(h);
+  if (lane == 0) {
+    const bool valid = ignore == nullptr || ignore[t] == 0;
+    const float coef = valid ? inv_tau * inv_nvalid[0] : 0.f;
+    rowM[r] = m;
+    rowH[r] = h;
+    rowCoef[r] = coef;
+    rowCoefM[r] = coef * m;
+  }
+}
+
+// ------------------------------------------------- logits + online LSE -----
+// Tile of z^T = W H_c^T (M = vocabulary, N = chunk tokens). Each lane holds 64
+// vocabulary values of 4 tokens; the per-token max and sum of 2^(y - max) of
+// y = z log2(e)/tau are reduced in registers, across the two half-waves, and
+// across the two waves sharing the tokens through LDS. Output per (token,
+// vocabulary tile): (max, sum) in base-2 units.
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict__ W,
+                                                            const T* __restrict__ Hc, int D,
+                                                            int V, int rows, int TM, int TN,
+                                                            float k2, float* part_m,
+                                                            float* part_s, int nVT) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
+  int mt, nt;
+  tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
+  const int m0 = mt * kTile, n0 = nt * kTile;
+  const int eb = Elt<T>::bytes;
+  const int ld = D * eb;
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  AccTile acc;
+  gemm_tile<T>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
+               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowBytes,
+               lds, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const bool full = m0 + kTile <= V;
+  float* xch = reinterpret_cast<float*>(lds);
+  float rm[4], rs[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const float y = acc.v[i][j][r] * k2;
+        if (full || v < V) mx = fmaxf(mx, y);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    float s = 0.f;
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const float e = fast_exp2(acc.v[i][j][r] * k2 - mx);
+          if (full || v < V) s += e;
+        }
+    }
+    s += __shfl_xor(s, 32);
+    rm[j] = mx;
+    rs[j] = s;
+    if (wm == 1 && lane < 32) {
+      xch[((wn * 4 + j) * 32 + lane) * 2 + 0] = mx;
+      xch[((wn * 4 + j) * 32 + lane) * 2 + 1] = s;
+    }
+  }
+  __syncthreads();
+  if (wm == 0 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = n0 + wn * 128 + 32 * j + lane;
+      const float m1 = rm[j], s1 = rs[j];
+      const float m2 = xch[((wn * 4 + j) * 32 + lane) * 2 + 0];
+      const float s2 = xch[((wn * 4 + j) * 32 + lane) * 2 + 1];
+      const float mm = fmaxf(m1, m2);
+      float ss = 0.f;
+      if (mm != -INFINITY) ss = s1 * fast_exp2(m1 - mm) + s2 * fast_exp2(m2 - mm);
+      if (t < rows) {
+        part_m[(int64_t)t * nVT + mt] = mm;
+        part_s[(int64_t)t * nVT + mt] = ss;
+      }
+    }
+  }
+}
+
+// log2 of the normaliser per token from the vocabulary-tile partials (fixed
+// order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau).
+__global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, int nVT,
+                            float* rowL2) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const float* pm = part_m + (int64_t)r * nVT;
+  const float* ps = part_s + (int64_t)r * nVT;
+  float mx = -INFINITY;
+  for (int j = lane; j < nVT; j += 64) mx = fmaxf(mx, pm[j]);
+  mx = wave_max(mx);
+  float s = 0.f;
+  for (int j = lane; j < nVT; j += 64) {
+    const float m = pm[j];
+    if (m != -INFINITY) s += ps[j] * fast_exp2(m - mx);
+  }
+  s = wave_sum(s);
+  if (lane == 0) rowL2[r] = mx + log2f(s);
+}
+
+// --------------------------------------- logit recompute + dZ epilogue -----
+// Same tile as k_logits_lse (bitwise identical z). The fp32 tile is staged in
+// LDS 128 tokens at a time as [token][vocab] with a 16-byte-slot swizzle. One
+// wave per token row: G = (g/tau) M 2^(y - L2) for the dense part, the K
+// teacher entries of the row that fall in this vocabulary tile are folded in
+// (G -= (g/tau) p; C += p z), then G is stored row-major to dZ[c, Vp] and,
+// after a barrier, column-major to dZ^T[Vp, cp]. Padded token rows produce
+// zeros so dZ^T's K padding for the dW GEMM is zero.
+__device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
+
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_dz(
+    const T* __restrict__ W, const T* __restrict__ Hc, int D, int V, int rows, int TM, int TN,
+    float k2, const float* __restrict__ rowL2, const float* __restrict__ rowCoef,
+    const float* __restrict__ rowCoefM, const int32_t* __restrict__ tidx,
+    const float* __restrict__ tp, int K, T* dZ, int64_t ldz, T* dZt, int64_t ldzt,
+    float* part_C, int nVT) {
+  constexpr int kStage = 128 * 256 * 4;  // 128 token rows x 256 vocab, fp32
+  __shared__ __attribute__((aligned(16))) char lds[kStage + 4 * 256 * 4];
+  int mt, nt;
+  tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
+  const int m0 = mt * kTile, n0 = nt * kTile;
+  const int eb = Elt<T>::bytes;
+  const int ld = D * eb;
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  AccTile acc;
+  gemm_tile<T>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
+               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowBytes,
+               lds, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  float* st = reinterpret_cast<float*>(lds);
+  float* corr = reinterpret_cast<float*>(lds + kStage) + wave * 256;
+  const int vl0 = 4 * lane;  // this lane's 4 vocabulary columns in the row pass
+  const bool vfull = m0 + kTile <= V;
+
+  for (int h = 0; h < 2; ++h) {
+    if (wn == h) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq) {
+            const int n = 32 * j + (lane & 31);
+            const int vl = wm * 128 + 32 * i + 8 * rq + 4 * (lane >> 5);
+            const int slot = (vl >> 2) ^ hsw16(n);
+            f32x4_t x = {acc.v[i][j][4 * rq + 0], acc.v[i][j][4 * rq + 1],
+                         acc.v[i][j][4 * rq + 2], acc.v[i][j][4 * rq + 3]};
+            *reinterpret_cast<f32x4_t*>(st + n * 256 + slot * 4) = x;
+          }
+    }
+    __syncthreads();
+
+    for (int rr = 0; rr < 32; ++rr) {
+      const int n = wave * 32 + rr;
+      const int tl = n0 + 128 * h + n;  // token row within the chunk
+      float* srow = st + n * 256;
+      const int myslot = lane ^ hsw16(n);
+      f32x4_t G = {0.f, 0.f, 0.f, 0.f};
+      if (tl < rows) {
+        const f32x4_t z = *reinterpret_cast<const f32x4_t*>(srow + myslot * 4);
+        const float cm = rowCoefM[tl], cf = rowCoef[tl], L2 = rowL2[tl];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool ok = vfull || (m0 + vl0 + e < V);
+          G[e] = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
+        }
+        // teacher entries of this row inside [m0, m0 + 256)
+        *reinterpret_cast<f32x4_t*>(corr + vl0) = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_wave_barrier();
+        float cpart = 0.f;
+        bool hit = false;
+        const int32_t* ir = tidx + (int64_t)tl * K;
+        const float* pr = tp + (int64_t)tl * K;
+        for (int kb = 0; kb < K; kb += 64) {
+          const int k = kb + lane;
+          if (k < K) {
+            const int dv = ir[k] - m0;
+            if (dv >= 0 && dv < kTile) {
+              const float pk = pr[k];
+              const float zv = srow[(((dv >> 2) ^ hsw16(n)) << 2) + (dv & 3)];
+              cpart += pk * zv;
+              corr[dv] = -cf * pk;
+              hit = true;
+            }
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (__any(hit)) {
+          const f32x4_t c = *reinterpret_cast<const f32x4_t*>(corr + vl0);
+          G += c;
+          cpart = wave_sum(cpart);
+        }
+        if (lane == 0) part_C[(int64_t)tl * nVT + mt] = cpart;
+        if (dZ != nullptr) {
+          T* dst = dZ + (int64_t)tl * ldz + m0 + vl0;
+          if constexpr (sizeof(T) == 2) {
+            u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
+            *reinterpret_cast<u32x2_t*>(dst) = pk2;
+          } else {
+            *reinterpret_cast<f32x4_t*>(dst) = G;
+          }
+        }
+      }
+      if (dZt != nullptr) *reinterpret_cast<f32x4_t*>(srow + myslot * 4) = G;
+    }
+    __syncthreads();
+
+    if (dZt != nullptr) {
+      // column-major store: lane -> (vocab column, 8 consecutive tokens)
+      const int q = lane & 15;
+#pragma unroll 4
+      for (int it = 0; it < 16; ++it) {
+        const int vl = it * 16 + wave * 4 + (lane >> 4);
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int n = 8 * q + e;
+          x[e] = st[n * 256 + ((((vl >> 2) ^ hsw16(n)) << 2) | (vl & 3))];
+        }
+        T* dst = dZt + (int64_t)(m0 + vl) * ldzt + n0 + 128 * h + 8 * q;
+        if constexpr (sizeof(T) == 2) {
+          u32x4_t w = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                       pack_bf16x2(x[6], x[7])};
+          *reinterpret_cast<u32x4_t*>(dst) = w;
+        } else {
+          *reinterpret_cast<f32x4_t*>(dst) = f32x4_t{x[0], x[1], x[2], x[3]};
+          *reinterpret_cast<f32x4_t*>(dst + 4) = f32x4_t{x[4], x[5], x[6], x[7]};
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2), 0 on ignored rows; per-block
+// partial sums in a fixed order for the deterministic mean.
+__global__ void k_row_loss(const float* part_C, int nVT, const float* rowL2, const float* rowM,
+                           const float* rowH, const float* rowCoef, int rows, float inv_tau,
+                           float* loss_per_token, float* block_partial) {
+  __shared__ float red[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float acc = 0.f;
+  for (int rr = 0; rr < 64; ++rr) {
+    const int r = blockIdx.x * 256 + wave * 64 + rr;
+    if (r >= rows) break;
+    const float* pc = part_C + (int64_t)r * nVT;
+    float c = 0.f;
+    for (int j = lane; j < nVT; j += 64) c += pc[j];
+    c = wave_sum(c);
+    const float l = rowCoef[r] != 0.f ? rowH[r] - c * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
+    if (lane == 0) {
+      if (loss_per_token) loss_per_token[r] = l;
+      acc += l;
+    }
+  }
+  if (lane == 0) red[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) block_partial[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ void k_finalize_loss(const float* partials, int n, const float* inv_nvalid,
+                                float* loss) {
+  __shared__ float red[256];
+  float s = 0.f;
+  for (int i = threadIdx.x; i < n; i += 256) s += partials[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) loss[0] = red[0] * inv_nvalid[0];
+}
+
+// --------------------------------------------------------------- transpose --
+// dst[C][ldd] <- src[R][lds_]^T for r < R, zero for R <= r < Rpad (64x64 tiles).
+template <typename T>
+__global__ void k_transpose_pad(const T* __restrict__ src, int64_t R, int64_t C, int64_t lds_,
+                                T* __restrict__ dst, int64_t ldd, int64_t Rpad) {
+  __shared__ T tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 256 threads: 64 x 4
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t r = r0 + y, c = c0 + tx;
+    tile[y][tx] = (r < R && c < C) ? src[r * lds_ + c] : (T)0.0f;
+  }
+  __syncthreads();
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t c = c0 + y, r = r0 + tx;
+    if (c < C && r < Rpad) dst[c * ldd + r] = tile[tx][y];
+  }
+}
+
+// -------------------------------------------------------------------- dH ----
+// dH_c[t, d] = sum_v dZ[t, v] W[v, d] as dZ[c, Vp] * (W^T[D, Vp])^T. With
+// split > 1 each split covers a K range and writes fp32 partials.
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, int64_t ldz,
+                                                    const T* __restrict__ Wt, int64_t ldw,
+                                                    int rows, int D, int TM, int TN, int ks_total,
+                                                    int split, T* gH, float* partial) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
+  const int tiles = TM * TN;
+  const int sidx = blockIdx.x / tiles;
+  int mt, nt;
+  tile_coords(blockIdx.x - sidx * tiles, TM, TN, 4, mt, nt);
+  const int m0 = mt * kTile, n0 = nt * kTile;
+  const int eb = Elt<T>::bytes;
+  const int lda = (int)(ldz * eb), ldb = (int)(ldw * eb);
+  const int per = (ks_total + split - 1) / split;
+  const int kb = sidx * per, ke = min(ks_total, kb + per);
+  AccTile acc;
+  const int mrows = min(kTile, rows - m0), nrows = min(kTile, D - n0);
+  gemm_tile<T>(make_rsrc(dZ + (int64_t)m0 * ldz, (uint32_t)(mrows * lda)), lda,
+               make_rsrc(Wt + (int64_t)n0 * ldw, (uint32_t)(nrows * ldb)), ldb, kb, ke, lds, acc);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int d = n0 + wn * 128 + 32 * j + (lane & 31);
+      if (d >= D) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int t = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (t < rows) {
+          if (split == 1)
+            gH[(int64_t)t * D + d] = (T)acc.v[i][j][r];
+          else
+            partial[((int64_t)sidx * rows + t) * D + d] = acc.v[i][j][r];
+        }
+      }
+    }
+}
+
+template <typename T>
+__global__ void k_dh_reduce(const float* partial, int split, int64_t n, T* gH) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) {
+    float s = 0.f;
+    for (int k = 0; k < split; ++k) s += partial[(int64_t)k * n + i];
+    gH[i] = (T)s;
+  }
+}
+
+// -------------------------------------------------------------------- dW ----
+// grad_W[v, d] (+)= sum_t dZ[t, v] H_c[t, d] as dZ^T[Vp, cp] * (H_c^T[D, cp])^T,
+// fp32 read-modify-write of the output tile when beta = 1.
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZt, int64_t ldzt,
+                                                    const T* __restrict__ Hct, int64_t ldh, int V,
+                                                    int D, int TM, int TN, int ks_total, int beta,
+                                                    float* __restrict__ gW) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
+  int mt, nt;
+  tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
+  const int m0 = mt * kTile, n0 = nt * kTile;
+  const int eb = Elt<T>::bytes;
+  const int lda = (int)(ldzt * eb), ldb = (int)(ldh * eb);
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, D - n0);
+  AccTile acc;
+  gemm_tile<T>(make_rsrc(dZt + (int64_t)m0 * ldzt, (uint32_t)(mrows * lda)), lda,
+               make_rsrc(Hct + (int64_t)n0 * ldh, (uint32_t)(nrows * ldb)), ldb, 0, ks_total, lds,
+               acc);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int d = n0 + wn * 128 + 32 * j + (lane & 31);
+      if (d >= D) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (v < V) {
+          float* o = gW + (int64_t)v * D + d;
+          *o = beta ? *o + acc.v[i][j][r] : acc.v[i][j][r];
+        }
+      }
+    }
+}
+
+// ------------------------------------------------------------ index check --
+// flag |= 1 if an index is outside [0, V); |= 2 if a row repeats an index.
+__global__ void k_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= N) return;
+  const int32_t* row = idx + r * K;
+  int bad = 0;
+  for (int k = lane; k < K; k += 64) {
+    const int32_t v = row[k];
+    if (v < 0 || (int64_t)v >= V) bad |= 1;
+    for (int k2 = k + 1; k2 < K; ++k2)
+      if (row[k2] == v) bad |= 2;
+  }
+  if (bad) atomicOr(flag, bad);
+}
+
+}  // namespace kd
+
+// ================================================================ launchers ==
+using namespace kd;
+
+static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+template <typename T>
+static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
+  const T* W = static_cast<const T*>(a.W);
+  const T* Hc = static_cast<const T*>(a.Hc);
+  const int TMv = cdiv(a.V, kTile), TNt = cdiv(a.rows, kTile);
+  const float k2 = kLog2e * a.inv_tau;
+
+  hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
+                     a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.inv_nvalid, a.p, a.rowM, a.rowH,
+                     a.rowCoef, a.rowCoefM);
+  hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
+                     (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT);
+  hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
+                     a.rows, a.nVT, a.rowL2);
+  hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
+                     a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.tidx, a.p, a.K,
+                     static_cast<T*>(a.dZ), a.ldz, static_cast<T*>(a.dZt), a.ldzt, a.part_C,
+                     a.nVT);
+  hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 256)), dim3(256), 0, s, a.part_C, a.nVT,
+                     a.rowL2, a.rowM, a.rowH, a.rowCoef, a.rows, a.inv_tau, a.loss_per_token,
+                     a.block_partial);
+  if (a.gH != nullptr) {
+    const int TM = cdiv(a.rows, kTile), TN = cdiv(a.D, kTile);
+    const int ks = (int)(a.ldz * sizeof(T) / kRowBytes);
+    hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.dh_split), dim3(kThreads), 0, s,
+                       static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.Wt), a.ldw,
+                       a.rows, (int)a.D, TM, TN, ks, a.dh_split, static_cast<T*>(a.gH),
+                       a.dh_partial);
+    if (a.dh_split > 1) {
+      const int64_t n = (int64_t)a.rows * a.D;
+      hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256),
+                         0, s, a.dh_partial, a.dh_split, n, static_cast<T*>(a.gH));
+    }
+  }
+  if (a.gW != nullptr) {
+    // grid covers the padded extent so H_c^T's K padding is written as zeros
+    hipLaunchKernelGGL(k_transpose_pad<T>, dim3(cdiv(a.ldh, 64), cdiv(a.D, 64)), dim3(256), 0,
+                       s, Hc, (int64_t)a.rows, a.D, a.D, static_cast<T*>(a.Hct), a.ldh,
+                       a.ldh);
+    const int TM = cdiv(a.V, kTile), TN = cdiv(a.D, kTile);
+    // K range = the chunk's token tiles (dZ^T columns past them are not written)
+    const int ks = (int)((int64_t)TNt * kTile * sizeof(T) / kRowBytes);
+    hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s,
+                       static_cast<const T*>(a.dZt), a.ldzt, static_cast<const T*>(a.Hct), a.ldh,
+                       (int)a.V, (int)a.D, TM, TN, ks, a.dw_beta, a.gW);
+  }
+  return (int)hipGetLastError();
+}
+
+extern "C" int kd_launch_chunk(const KdChunkArgs* a, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return a->dtype == 1 ? launch_chunk_impl<__bf16>(*a, s) : launch_chunk_impl<float>(*a, s);
+}
+
+extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(256), 0, s, a->ignore, a->N, a->nvalid,
+                     a->inv_nvalid);
+  if (a->Wt != nullptr) {
+    const dim3 grid(cdiv(a->ldw, 64), cdiv(a->D, 64));  // includes the zero padding
+    if (a->dtype == 1)
+      hipLaunchKernelGGL(k_transpose_pad<__bf16>, grid, dim3(256), 0, s,
+                         static_cast<const __bf16*>(a->W), a->V, a->D, a->D,
+                         static_cast<__bf16*>(a->Wt), a->ldw, a->ldw);
+    else
+      hipLaunchKernelGGL(k_transpose_pad<float>, grid, dim3(256), 0, s,
+                         static_cast<const float*>(a->W), a->V, a->D, a->D,
+                         static_cast<float*>(a->Wt), a->ldw, a->ldw);
+  }
+  if (a->zero_gW != nullptr) {
+    const int64_t n = a->V * a->D;
+    hipLaunchKernelGGL(k_fill_f32, dim3(std::min<int64_t>(cdiv(n, 256), 16384)), dim3(256), 0, s,
+                       a->zero_gW, n, 0.0f);
+  }
+  return (int)hipGetLastError();
+}
+
+extern "C" int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid,
+                                  float* loss, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(k_finalize_loss, dim3(1), dim3(256), 0, s, partials, n, inv_nvalid, loss);
+  return (int)hipGetLastError();
+}
+
+extern "C" int kd_launch_check_indices(const int32_t* idx, int64_t N, int K, int64_t V,
+                                       int* flag, int* host_flag, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemsetAsync(flag, 0, sizeof(int), s);
+  if (e != hipSuccess) return (int)e;
+  if (N > 0)
+    hipLaunchKernelGGL(k_check_indices, dim3(cdiv(N, 4)), dim3(256), 0, s, idx, N, K, V, flag);
+  e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  e = hipMemcpyAsync(host_flag, flag, sizeof(int), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return (int)e;
+  return (int)hipStreamSynchronize(s);
+}

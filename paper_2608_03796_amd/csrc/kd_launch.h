@@ -1,0 +1,63 @@
+// Internal interface between the host scheduler (kd_api.cpp, plain C++) and
+// the HIP launchers (kd_kernels.hip). No HIP types: streams travel as void*.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+struct KdPrepareArgs {
+  int dtype;                // 0 fp32, 1 bf16
+  int64_t N, D, V;
+  const uint8_t* ignore;    // [N] or null
+  int* nvalid;              // device int
+  float* inv_nvalid;        // device float: 1/N_valid or 0
+  const void* W;            // [V, D]
+  void* Wt;                 // [D, ldw] or null (no dH requested)
+  int64_t ldw;              // padded vocabulary (multiple of 256)
+  float* zero_gW;           // grad_W to clear, or null
+};
+
+struct KdChunkArgs {
+  int dtype;
+  int64_t D, V;
+  int K;
+  int64_t row0;             // first token of the chunk
+  int rows;                 // tokens in the chunk
+  float inv_tau;
+  const void* W;            // [V, D]
+  const void* Hc;           // hidden + row0 * D
+  const int32_t* tidx;      // teacher_idx + row0 * K
+  const float* tlogit;      // full [N, K] (prologue indexes with row0)
+  const uint8_t* ignore;    // full [N] or null
+  const float* inv_nvalid;
+  // per-chunk workspace
+  float* p;                 // [rows, K]
+  float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
+  float *part_m, *part_s, *part_C;                   // [rows, nVT]
+  int nVT;
+  void* dZ;                 // [cp, ldz] or null (no dH)
+  int64_t ldz;              // = padded vocabulary
+  void* dZt;                // [ldz, ldzt] or null (no dW)
+  int64_t ldzt;             // = padded chunk
+  void* Hct;                // [D, ldh] or null (no dW)
+  int64_t ldh;              // = padded chunk
+  const void* Wt;           // [D, ldw] (dH)
+  int64_t ldw;
+  int dh_split;
+  float* dh_partial;        // [dh_split, rows, D] when dh_split > 1
+  // outputs
+  float* loss_per_token;    // + row0, or null
+  float* block_partial;     // this chunk's cdiv(rows, 256) partial sums
+  void* gH;                 // grad_hidden + row0 * D, or null
+  float* gW;                // grad_W or null
+  int dw_beta;              // 0 overwrite, 1 accumulate
+};
+
+extern "C" {
+int kd_launch_prepare(const KdPrepareArgs* a, void* stream);
+int kd_launch_chunk(const KdChunkArgs* a, void* stream);
+int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid, float* loss,
+                       void* stream);
+int kd_launch_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag,
+                            int* host_flag, void* stream);
+}

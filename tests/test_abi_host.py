@@ -1,0 +1,154 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library is loaded with ctypes; every argument error is detected on the host
+before anything is enqueued, so each error code can be forced here with fake
+(never dereferenced) device pointers. A call that would pass validation is never
+made in this file.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_03796_amd as kd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kdtopk.h")
+
+FAKE = 0x10000          # 16-byte aligned, never dereferenced
+FAKE_MISALIGNED = 0x10008
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return kd.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:kd_status|const char\*|int)\s+(kd_\w+)\s*\(", text, re.M))
+    assert declared == set(kd.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_abi_version(lib):
+    text = open(HEADER).read()
+    v = int(re.search(r"#define KDTOPK_ABI_VERSION (\d+)", text).group(1))
+    assert lib.kd_abi_version() == v
+
+
+def test_status_strings(lib):
+    for code, name in kd.STATUS.items():
+        assert lib.kd_status_string(code).decode().startswith(name)
+    assert lib.kd_status_string(99) == b"unknown kd_status"
+
+
+def _prob(**kw):
+    base = dict(N=256, D=256, V=4096, K=16, chunk=64, tau=1.0, dtype=kd.KD_F32)
+    base.update(kw)
+    return kd.problem(base["N"], base["D"], base["V"], base["K"], base["chunk"], base["tau"],
+                      base["dtype"], base.get("flags", 0))
+
+
+def _ws(lib, pr):
+    out = ctypes.c_size_t(0)
+    rc = lib.kd_topk_kl_workspace_size(ctypes.byref(pr), ctypes.byref(out))
+    return rc, out.value
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(N=-1), 2), (dict(N=2 ** 31), 2), (dict(D=0), 2), (dict(D=32), 2), (dict(D=65600), 2),
+    (dict(D=96), 4), (dict(V=0), 2), (dict(V=2 ** 20 + 1), 2), (dict(K=0), 2),
+    (dict(K=4097), 2), (dict(chunk=0), 3), (dict(chunk=-5), 3), (dict(tau=0.0), 3),
+    (dict(tau=-1.0), 3), (dict(tau=float("inf")), 3), (dict(tau=float("nan")), 3),
+    (dict(dtype=2), 4), (dict(dtype=-1), 4), (dict(flags=1), 3),
+])
+def test_workspace_size_rejects(lib, kw, code):
+    rc, _ = _ws(lib, _prob(**kw))
+    assert rc == code
+
+
+def test_workspace_size_null(lib):
+    pr = _prob()
+    assert lib.kd_topk_kl_workspace_size(None, ctypes.byref(ctypes.c_size_t())) == 1
+    assert lib.kd_topk_kl_workspace_size(ctypes.byref(pr), None) == 1
+
+
+def test_workspace_linear_not_nv(lib):
+    """The workspace grows with N only through per-256-row loss partials."""
+    sizes = {}
+    for N in (4096, 32768, 262144):
+        rc, b = _ws(lib, _prob(N=N, D=4096, V=131072, K=100, chunk=4096, dtype=kd.KD_BF16))
+        assert rc == 0
+        sizes[N] = b
+    assert sizes[262144] - sizes[4096] < 4096  # bytes, not N*V
+    assert sizes[4096] < 8 * 2 ** 30
+    # N*V bf16 logits at 256K tokens would be 64 GiB
+    assert sizes[262144] < 262144 * 131072 * 2 / 8
+
+
+def test_workspace_chunk_clamped_to_N(lib):
+    rc1, a = _ws(lib, _prob(N=100, chunk=100))
+    rc2, b = _ws(lib, _prob(N=100, chunk=10 ** 6))
+    assert rc1 == rc2 == 0 and a == b
+
+
+def _call(lib, pr, hidden=FAKE, W=FAKE, idx=FAKE, logit=FAKE, ignore=None, loss=FAKE,
+          lpt=None, gh=FAKE, gw=FAKE, acc=0, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        rc, ws_bytes = _ws(lib, pr)
+        if rc != 0:
+            ws_bytes = 1 << 40
+    v = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.kd_topk_kl_fwd_bwd(ctypes.byref(pr), v(hidden), v(W), v(idx), v(logit), v(ignore),
+                                  v(loss), v(lpt), v(gh), v(gw), acc, v(ws),
+                                  ctypes.c_size_t(ws_bytes), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(N=-3), 2), (dict(D=100), 4), (dict(K=5000), 2), (dict(chunk=0), 3),
+    (dict(tau=0.0), 3), (dict(dtype=7), 4), (dict(flags=2), 3),
+])
+def test_fwd_bwd_rejects_problem(lib, kw, code):
+    assert _call(lib, _prob(**kw)) == code
+
+
+@pytest.mark.parametrize("field", ["hidden", "W", "idx", "logit", "loss", "ws"])
+def test_fwd_bwd_null_pointers(lib, field):
+    assert _call(lib, _prob(), **{field: None}) == 1
+
+
+def test_fwd_bwd_problem_null(lib):
+    v = ctypes.c_void_p(FAKE)
+    assert lib.kd_topk_kl_fwd_bwd(None, v, v, v, v, None, v, None, v, v, 0, v,
+                                  ctypes.c_size_t(1 << 40), None) == 1
+
+
+@pytest.mark.parametrize("field", ["hidden", "W", "gh", "gw", "ws"])
+def test_fwd_bwd_misaligned(lib, field):
+    assert _call(lib, _prob(), **{field: FAKE_MISALIGNED}) == 4
+
+
+@pytest.mark.parametrize("acc", [2, -1])
+def test_fwd_bwd_bad_accumulate(lib, acc):
+    assert _call(lib, _prob(), acc=acc) == 3
+
+
+def test_fwd_bwd_workspace_too_small(lib):
+    pr = _prob()
+    rc, need = _ws(lib, pr)
+    assert rc == 0 and need > 0
+    assert _call(lib, pr, ws_bytes=need - 1) == 5
+
+
+def test_check_indices_rejects(lib):
+    pr = _prob(K=0)
+    assert lib.kd_topk_kl_check_indices(ctypes.byref(pr), ctypes.c_void_p(FAKE),
+                                        ctypes.c_void_p(FAKE), ctypes.c_size_t(1 << 40), None) == 2
+    pr = _prob()
+    assert lib.kd_topk_kl_check_indices(ctypes.byref(pr), None, ctypes.c_void_p(FAKE),
+                                        ctypes.c_size_t(1 << 40), None) == 1
+    assert lib.kd_topk_kl_check_indices(ctypes.byref(pr), ctypes.c_void_p(FAKE),
+                                        ctypes.c_void_p(FAKE), ctypes.c_size_t(16), None) == 5

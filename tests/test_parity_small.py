@@ -1,0 +1,178 @@
+"""GPU parity at sizes the oracle finishes in seconds: every element of the
+loss, per-token loss and both gradients against the fp64 oracle on the same
+seeded inputs. Shapes span several 256x256 tiles with ragged tails in N, V and
+the chunk, plus the method's degenerate cases."""
+import numpy as np
+import pytest
+import torch
+
+import kd_inputs as ki
+from oracle import kd_topk_kl
+from tests.helpers import TOL, oracle_inputs, rel_max, to64
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(N, D, V, K, dtype, seed=0, ignore_frac=0.0, wstd=0.02, hstd=1.0):
+    dev = "cuda"
+    hidden = ki.make_hidden(N, D, dtype, dev, seed=ki.SEED_HIDDEN + seed, std=hstd)
+    W = ki.make_weight(V, D, dtype, dev, seed=ki.SEED_W + seed, std=wstd)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + seed)
+    ignore = None
+    if ignore_frac > 0:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(ki.SEED_MASK + seed)
+        ignore = (torch.rand(N, generator=g) < ignore_frac).to(torch.uint8).to(dev)
+    return dict(hidden=hidden, W=W, teacher_idx=idx, teacher_logit=logit, ignore=ignore)
+
+
+def _run_and_compare(kd, inp, tau, chunk, tol, grads=True):
+    torch.cuda.synchronize()
+    out = kd.fwd_bwd(inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"], tau=tau,
+                     ignore=inp["ignore"], chunk=chunk, loss_per_token=True,
+                     grad_hidden=grads, grad_W=grads)
+    torch.cuda.synchronize()
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk, want_grads=grads)
+    loss = float(out["loss"])
+    assert np.isfinite(loss)
+    assert abs(loss - ref["loss"]) <= tol["loss"] * max(abs(ref["loss"]), 1e-30), (loss, ref["loss"])
+    lpt = to64(out["loss_per_token"])
+    assert rel_max(lpt, ref["loss_per_token"]) <= tol["loss"]
+    if grads:
+        assert rel_max(to64(out["grad_hidden"]), ref["grad_hidden"]) <= tol["grad"]
+        assert rel_max(to64(out["grad_W"]), ref["grad_W"]) <= tol["grad"]
+    return out, ref
+
+
+def test_tiny_fp32_workload(gpu_lib):
+    """N=256, D=256, V=4096, K=16, chunk 64, tau 1, fp32."""
+    w = ki.WORKLOADS["tiny_fp32"]
+    inp = ki.make_workload_inputs(w, "cuda")
+    _run_and_compare(gpu_lib, inp, w.tau, w.chunk, TOL["f32"])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,D,V,K,chunk,tau,ign", [
+    (259, 128, 4133, 7, 100, 2.0, 0.2),      # ragged N, V, chunk; tau 2; mask
+    (513, 192, 1000, 16, 513, 1.0, 0.0),     # one chunk, V < 4 tiles, D not /256
+    (300, 64, 777, 1, 64, 0.5, 0.1),         # K = 1, tau < 1
+    (64, 256, 2048, 40, 1000, 1.0, 0.0),     # chunk > N
+])
+def test_ragged_shapes(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=N + V, ignore_frac=ign)
+    _run_and_compare(gpu_lib, inp, tau, chunk, TOL[dtype])
+
+
+def test_k_equals_v(gpu_lib):
+    """The support is the whole vocabulary (P4 structure) on the GPU."""
+    inp = _inputs(96, 64, 320, 320, torch.float32, seed=5)
+    _run_and_compare(gpu_lib, inp, 1.0, 32, TOL["f32"])
+
+
+def test_identity_head_kl_zero(gpu_lib):
+    """W = I (D = V): hidden are the logits; teacher reproduced on its support
+    and -1e4 elsewhere gives l = 0 and zero gradients (P2)."""
+    V, K, N = 256, 12, 40
+    idx, logit = ki.make_teacher(N, K, V, "cuda", seed=77)
+    hidden = torch.full((N, V), -1e4, dtype=torch.float32, device="cuda")
+    hidden.scatter_(1, idx.long(), logit)
+    W = torch.eye(V, dtype=torch.float32, device="cuda")
+    out = gpu_lib.fwd_bwd(hidden, W, idx, logit, tau=1.0, chunk=16, loss_per_token=True)
+    torch.cuda.synchronize()
+    assert abs(float(out["loss"])) < 1e-5
+    assert float(out["grad_hidden"].abs().max()) < 1e-6
+
+
+def test_identity_head_closed_form_gradient(gpu_lib):
+    """W = I: grad_hidden is the logit gradient g/tau (M q - p) itself (P6)."""
+    V, K, N, tau = 512, 9, 70, 2.0
+    inp = _inputs(N, V, V, K, torch.float32, seed=8, hstd=3.0)
+    inp["W"] = torch.eye(V, dtype=torch.float32, device="cuda")
+    _run_and_compare(gpu_lib, inp, tau, 32, TOL["f32"])
+
+
+def test_all_ignored(gpu_lib):
+    inp = _inputs(200, 64, 600, 5, torch.float32, seed=9)
+    inp["ignore"] = torch.ones(200, dtype=torch.uint8, device="cuda")
+    out = gpu_lib.fwd_bwd(inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"],
+                          ignore=inp["ignore"], chunk=64, loss_per_token=True)
+    torch.cuda.synchronize()
+    assert float(out["loss"]) == 0.0
+    assert float(out["grad_hidden"].abs().max()) == 0.0
+    assert float(out["grad_W"].abs().max()) == 0.0
+    assert float(out["loss_per_token"].abs().max()) == 0.0
+
+
+def test_empty_batch(gpu_lib):
+    D, V, K = 64, 300, 4
+    hidden = torch.empty(0, D, device="cuda")
+    W = ki.make_weight(V, D, torch.float32, "cuda")
+    idx = torch.empty(0, K, dtype=torch.int32, device="cuda")
+    logit = torch.empty(0, K, dtype=torch.float32, device="cuda")
+    gW = torch.full((V, D), 7.0, device="cuda")
+    out = gpu_lib.fwd_bwd(hidden, W, idx, logit, chunk=16, grad_W_out=gW)
+    torch.cuda.synchronize()
+    assert float(out["loss"]) == 0.0
+    assert float(gW.abs().max()) == 0.0
+
+
+def test_accumulate_grad_W(gpu_lib):
+    inp = _inputs(150, 64, 700, 6, torch.float32, seed=10)
+    a = gpu_lib.fwd_bwd(inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"],
+                        chunk=64)
+    gW = a["grad_W"].clone()
+    gpu_lib.fwd_bwd(inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"], chunk=64,
+                    grad_W_out=gW, accumulate_grad_W=True, grad_hidden=False)
+    torch.cuda.synchronize()
+    assert rel_max(to64(gW), 2 * to64(a["grad_W"])) <= 1e-6
+
+
+def test_forward_only_and_partial_grads(gpu_lib):
+    inp = _inputs(260, 128, 900, 8, torch.bfloat16, seed=11, ignore_frac=0.1)
+    args = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+    full = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=100)
+    fwd = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=100, grad_hidden=False, grad_W=False)
+    gh = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=100, grad_W=False)
+    gw = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=100, grad_hidden=False)
+    torch.cuda.synchronize()
+    assert float(fwd["loss"]) == float(full["loss"])
+    assert torch.equal(gh["grad_hidden"], full["grad_hidden"])
+    assert torch.equal(gw["grad_W"], full["grad_W"])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_deterministic(gpu_lib, dtype):
+    inp = _inputs(600, 128, 3000, 10, dtype, seed=12, ignore_frac=0.05)
+    args = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+    a = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=256, loss_per_token=True)
+    b = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=256, loss_per_token=True)
+    torch.cuda.synchronize()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("chunk", [7, 64, 259, 300])
+def test_chunk_invariance(gpu_lib, chunk):
+    inp = _inputs(259, 64, 1500, 6, torch.float32, seed=13, ignore_frac=0.1)
+    args = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+    ref = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=259)
+    out = gpu_lib.fwd_bwd(*args, ignore=inp["ignore"], chunk=chunk)
+    torch.cuda.synchronize()
+    assert abs(float(out["loss"]) - float(ref["loss"])) <= 1e-6 * abs(float(ref["loss"]))
+    assert rel_max(to64(out["grad_hidden"]), to64(ref["grad_hidden"])) <= 1e-6
+    assert rel_max(to64(out["grad_W"]), to64(ref["grad_W"])) <= 1e-6
+
+
+def test_check_indices(gpu_lib):
+    idx, _ = ki.make_teacher(300, 20, 1000, "cuda", seed=14)
+    assert gpu_lib.check_indices(idx, V=1000)
+    bad = idx.clone()
+    bad[17, 3] = 1000
+    assert not gpu_lib.check_indices(bad, V=1000)
+    bad = idx.clone()
+    bad[5, 0] = -1
+    assert not gpu_lib.check_indices(bad, V=1000)
+    dup = idx.clone()
+    dup[123, 7] = dup[123, 2]
+    assert not gpu_lib.check_indices(dup, V=1000)
