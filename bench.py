@@ -1,0 +1,156 @@
+#!/usr/bin/env python3
+"""Throughput of the fused chunked top-K KL loss (forward + backward) on one MI355X.
+
+One step = one kd_topk_kl_fwd_bwd call over the whole workload: teacher
+prologue, the chunked logits / online log-normaliser, the logit recompute with
+the closed-form gradient, and the dH and dW contractions, for every chunk.
+Inputs are synthetic (seeded) and resident in HBM before the timed region.
+
+Prints one JSON line. `roofline` is for the kernel with the largest total time,
+from HIP events the library records around each of its launches during the
+timed region; `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+METRIC = "fwd+bwd tokens/s of fused top-K KL loss (N=32K,D=4096,V=131K); MFMA %"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 (matrix and vector)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="loss32k",
+                    help="tiny_fp32 | loss4k | loss32k | packed | long256k")
+    ap.add_argument("--cpu-rows", type=int, default=512,
+                    help="token rows of the oracle's CPU baseline sample (0 = skip)")
+    ap.add_argument("--json-out", default=None, help="also append the JSON line to this file")
+    return ap.parse_args()
+
+
+def cpu_baseline(inp, w, rows_count):
+    """fp64 oracle (fwd+bwd) on a random sub-batch of `rows_count` tokens at
+    full D and V, timed on this host's cores."""
+    import numpy as np
+    import torch
+    import kd_inputs as ki
+    from oracle import kd_topk_kl
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()
+                     if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    sel = ki.sub_batch(w.N, rows_count).to(inp["hidden"].device)
+    h = inp["hidden"].index_select(0, sel).float().cpu().numpy()
+    W = inp["W"].float().cpu().numpy()
+    idx = inp["teacher_idx"].index_select(0, sel).cpu().numpy()
+    tl = inp["teacher_logit"].index_select(0, sel).cpu().numpy()
+    ign = None
+    if inp["ignore"] is not None:
+        ign = inp["ignore"].index_select(0, sel).cpu().numpy()
+    t0 = time.perf_counter()
+    res = kd_topk_kl(h, W, idx, tl, tau=w.tau, ignore=ign, chunk=256, want_grads=True)
+    dt = time.perf_counter() - t0
+    assert np.isfinite(res["loss"])
+    return {"value": rows_count / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{rows_count}-token random sub-batch (seed {ki.SEED_SUBBATCH}) of the "
+                      f"{w.name} workload at full D={w.D}, V={w.V}, K={w.K}; fp64 NumPy "
+                      f"forward+backward, dense logits per 256-row chunk; {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} is not supported: this build runs the loss on one "
+              f"GPU only (no collectives); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import kd_inputs as ki
+    import paper_2608_03796_amd as kd
+
+    kd.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = ki.WORKLOADS[args.workload]
+    print(f"bench: workload {w.name} N={w.N} D={w.D} V={w.V} K={w.K} chunk={w.chunk} "
+          f"tau={w.tau} {w.dtype}", file=sys.stderr, flush=True)
+    torch.cuda.reset_peak_memory_stats(dev)
+    inp = ki.make_workload_inputs(w, dev)
+    dt_code = kd.KD_BF16 if w.dtype == "bf16" else kd.KD_F32
+    ws = kd.alloc_workspace(w.N, w.D, w.V, w.K, w.chunk, w.tau, dt_code, dev)
+    out = {"loss": torch.empty((), dtype=torch.float32, device=dev),
+           "grad_hidden": torch.empty(w.N, w.D, dtype=w.torch_dtype, device=dev),
+           "grad_W": torch.empty(w.V, w.D, dtype=torch.float32, device=dev)}
+
+    def step():
+        kd.fwd_bwd(inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"], tau=w.tau,
+                   ignore=inp["ignore"], chunk=w.chunk, workspace=ws, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("bench: warmup done", file=sys.stderr, flush=True)
+    kd.profile_read()
+    kd.profile_enable(True)
+    stream = torch.cuda.current_stream(dev)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    kd.profile_enable(False)
+    prof = kd.profile_read()
+    ms = e0.elapsed_time(e1) / args.steps
+    peak_alloc = torch.cuda.max_memory_allocated(dev)
+    loss = float(out["loss"])
+    print(f"bench: {ms:.3f} ms/step, loss {loss:.6f}", file=sys.stderr, flush=True)
+
+    tokens_per_s = w.N / (ms / 1e3)
+    step_flops = 8.0 * w.N * w.D * w.V
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    dom_name, dom = max(prof.items(), key=lambda kv: kv[1]["total_ms"])
+    achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12 if dom["total_ms"] > 0 else 0.0
+    roofline = {"bound": "mfma", "kernel": dom_name, "achieved": round(achieved, 2),
+                "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "traffic": None,
+                "avg_launch_ms": round(dom["total_ms"] / dom["launches"], 4),
+                "flop_per_launch": dom["flops"] / dom["launches"]}
+    kernels = {k: {"launches": v["launches"], "ms_per_step": round(v["total_ms"] / args.steps, 4),
+                   "tflops": (round(v["flops"] / (v["total_ms"] / 1e3) / 1e12, 2)
+                              if v["flops"] and v["total_ms"] > 0 else None)}
+               for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["total_ms"])}
+    rec = {
+        "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": w.name, "N": w.N, "D": w.D, "V": w.V, "K": w.K, "chunk": w.chunk,
+                   "tau": w.tau, "ignored_frac": 0.05 if w.mask == "packed5" else 0.0},
+        "mfma_pct_of_step": round(100.0 * step_flops / (ms / 1e3) / (peak * 1e12), 2),
+        "peak_alloc_bytes": int(peak_alloc),
+        "loss": loss,
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    if args.cpu_rows > 0:
+        print("bench: timing the CPU oracle baseline", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline(inp, w, args.cpu_rows)
+    line = json.dumps(rec)
+    print(line, flush=True)
+    if args.json_out:
+        with open(args.json_out, "a") as f:
+            f.write(line + "\n")
+
+
+if __name__ == "__main__":
+    main()

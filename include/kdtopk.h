@@ -64,7 +64,7 @@ typedef enum kd_dtype {
 typedef struct kd_problem {
   int64_t N;           /* tokens = rows of hidden; 0 <= N < 2^31            */
   int64_t D;           /* hidden size d; 64 <= D <= 65536, D % 64 == 0       */
-  int64_t V;           /* vocabulary size; 1 <= V <= 4194304                 */
+  int64_t V;           /* vocabulary size; 1 <= V <= 1048576                 */
   int64_t chunk;       /* rows per chunk C_s; >= 1 (min(chunk, N) is used)   */
   int32_t K;           /* cached teacher entries per token; 1 <= K <= V      */
   int32_t dtype;       /* kd_dtype of hidden, W and grad_hidden              */
@@ -139,6 +139,26 @@ kd_status kd_topk_kl_check_indices(const kd_problem* p,
                                    void* workspace,
                                    size_t workspace_bytes,
                                    void* hip_stream);
+
+/*
+ * Instrumentation, not part of the method: per-kernel timing with HIP events.
+ * While enabled (process-wide), kd_topk_kl_fwd_bwd records a HIP event pair on
+ * its stream around each kernel launch; kd_profile_read waits for the recorded
+ * events, writes up to `max` entries (one per kernel kind that ran), clears the
+ * records and returns the number of entries written (negative on a HIP error).
+ * `flops` is the algorithmic floating-point work of the recorded launches (the
+ * four 2*rows*D*V contractions of each chunk; 0 for the other kernels).
+ * Creating events is an allocation: leave profiling off where that matters.
+ */
+typedef struct kd_kernel_time {
+  char name[32];       /* kernel kind, e.g. "logits_lse", "dz", "dh", "dw" */
+  int64_t launches;
+  double total_ms;     /* sum of event-measured durations */
+  double flops;        /* sum of algorithmic FLOP over the launches */
+} kd_kernel_time;
+
+kd_status kd_profile_enable(int on);
+int kd_profile_read(kd_kernel_time* out, int max);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char* kd_status_string(int status);

@@ -23,7 +23,7 @@ STATUS = {
     7: "KD_ERR_DEVICE",
 }
 EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_check_indices",
-            "kd_status_string", "kd_abi_version")
+            "kd_status_string", "kd_abi_version", "kd_profile_enable", "kd_profile_read")
 
 
 class KdError(RuntimeError):
@@ -36,6 +36,11 @@ class KdProblem(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("D", ctypes.c_int64), ("V", ctypes.c_int64),
                 ("chunk", ctypes.c_int64), ("K", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("temperature", ctypes.c_float), ("flags", ctypes.c_int32)]
+
+
+class KdKernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double), ("flops", ctypes.c_double)]
 
 
 _lib = None
@@ -62,6 +67,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.kd_status_string.restype = ctypes.c_char_p
     lib.kd_abi_version.argtypes = []
     lib.kd_abi_version.restype = ctypes.c_int
+    lib.kd_profile_enable.argtypes = [ctypes.c_int]
+    lib.kd_profile_enable.restype = ctypes.c_int
+    lib.kd_profile_read.argtypes = [ctypes.POINTER(KdKernelTime), ctypes.c_int]
+    lib.kd_profile_read.restype = ctypes.c_int
     if path is None:
         _lib = lib
     return lib
@@ -186,3 +195,19 @@ def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, work
     if rc != 0:
         raise KdError(rc, "kd_topk_kl_check_indices")
     return True
+
+
+def profile_enable(on: bool = True):
+    """Per-kernel HIP-event timing inside the library (instrumentation)."""
+    load_library().kd_profile_enable(int(bool(on)))
+
+
+def profile_read() -> dict:
+    """{kernel kind: {launches, total_ms, flops}} recorded since the last read."""
+    arr = (KdKernelTime * 32)()
+    n = load_library().kd_profile_read(arr, 32)
+    if n < 0:
+        raise KdError(7, "kd_profile_read")
+    return {arr[i].name.decode(): dict(launches=int(arr[i].launches),
+                                       total_ms=float(arr[i].total_ms),
+                                       flops=float(arr[i].flops)) for i in range(n)}

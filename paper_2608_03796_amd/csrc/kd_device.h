@@ -22,9 +22,8 @@ typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2_t;
 
 constexpr int kTile = 256;                       // BM = BN
 constexpr int kThreads = 256;                    // 4 waves of 64, 2 x 2
-constexpr int kRowBytes = 128;                   // one tile row per K step
-constexpr int kStageBytes = kTile * kRowBytes;   // 32 KiB per operand
-constexpr int kLdsMain = 4 * kStageBytes;        // A, B x 2 stages = 128 KiB
+constexpr int kRowB = 64;                        // bytes of a tile row per K step
+constexpr int kStages = 5;                       // LDS stages of the main loop
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -35,10 +34,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                            kRsrcWord3);
 }
-
-// 16-byte slot swizzle of the main-loop tiles (8 slots per 128-byte row):
-// conflict-free for the row-parallel LDS writes and the MFMA fragment reads.
-__device__ __forceinline__ int swz8(int row) { return (row ^ (row >> 3)) & 7; }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (pid % 8). Give each
 // XCD a contiguous range of the linear tile order, so the ~32 tiles an XCD runs
@@ -96,15 +91,50 @@ struct AccTile {
 };
 
 // One 256x256 output tile: acc = A[m0:m0+256, k-range] * B[n0:n0+256, k-range]^T.
+//
 // ra / rb are buffer resources based at the tile's first row, sized so rows
-// outside the operand read as zero (hardware range check). K steps are 128
-// bytes of a row (64 bf16 or 32 fp32). Double-buffered LDS, one barrier per
-// K step; the caller's LDS must hold kLdsMain bytes. Ends with a barrier, so
-// the caller may reuse the LDS.
-template <typename T>
+// outside the operand read as zero (hardware range check). A K step is ROWB
+// bytes of every row (ROWB = 64: 32 bf16 / 16 fp32). Operands go straight from
+// memory into LDS (buffer loads with the LDS-DMA bit: no VGPR staging, no
+// ds_write) through S stages, so S-1 K steps of operand data are in flight
+// while one is consumed; one barrier per K step. The MFMA fragments of the
+// next K sub-step are read while the current sub-step's MFMAs run. The
+// caller's LDS must hold gemm_lds_bytes<ROWB, S>() bytes. Ends with a barrier,
+// so the caller may reuse the LDS.
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int ROWB, int S>
+constexpr int gemm_lds_bytes() { return S * 2 * kTile * ROWB; }
+constexpr int kLdsMain = gemm_lds_bytes<kRowB, kStages>();  // 160 KiB
+
+// 16-byte slot swizzle of a ROWB-byte tile row: conflict-free for the DMA
+// rows and for 8- or 16-lane groups of MFMA fragment reads.
+template <int ROWB>
+__device__ __forceinline__ int slot_swz(int row) {
+  if constexpr (ROWB == 128) return (row ^ (row >> 3)) & 7;
+  else return ((row >> 1) ^ (row >> 3)) & 3;
+}
+
+// s_waitcnt vmcnt(n) for a compile-time n; expcnt/lgkmcnt are not waited.
+#define KD_VMCNT(n) __builtin_amdgcn_s_waitcnt((0x0f70 & ~0x000f) | ((n) & 0xf) | (((n) >> 4) << 14))
+template <typename T, int ROWB = kRowB, int S = kStages>
 __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_bytes,
                                           __amdgpu_buffer_rsrc_t rb, int ldb_bytes, int ks_begin,
                                           int ks_end, char* lds, AccTile& acc) {
+  constexpr int SL = ROWB / 16;           // 16-byte slots per row
+  constexpr int SUB = SL / 2;             // MFMA sub-steps per K step
+  constexpr int OPB = kTile * ROWB;       // one operand's stage
+  constexpr int STB = 2 * OPB;            // one stage (A and B)
+  constexpr int RPI = 1024 / ROWB;        // rows per 1 KiB DMA instruction
+  constexpr int NDMA = kTile / RPI / 4;   // DMA instructions per operand per wave
+  constexpr int NI = 2 * NDMA;            // per K step per wave (vmcnt units)
+  static_assert(SUB >= 2, "two or more sub-steps per K step");
+  static_assert((S - 1) * NI <= 63, "vmcnt range of the in-flight DMA steps");
+  static_assert(2 * NDMA <= 16, "one MFMA per DMA instruction in the last sub-step");
+  static_assert(NDMA <= 8, "DMA offsets array");
+  // (arrays captured by the lambdas below have literal bounds: clang's host
+  // pass rejects a second instantiation when the bound is a dependent local)
+
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -117,86 +147,124 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc.v[i][j][r] = 0.0f;
 
-  if (ks_end <= ks_begin) {
+  const int nsteps = ks_end - ks_begin;
+  if (nsteps <= 0) {
     __syncthreads();
     return;
   }
 
-  // global -> LDS: thread loads slot (tid&7) of rows (tid>>3) + 32*i
-  const int lrow = tid >> 3;
-  const int lslot = tid & 7;
-  // byte offsets are unsigned 32-bit (the buffer instruction's offset type)
-  const uint32_t voffA = (uint32_t)lrow * (uint32_t)lda_bytes + lslot * 16u;
-  const uint32_t voffB = (uint32_t)lrow * (uint32_t)ldb_bytes + lslot * 16u;
-  int ldsw[8];
+  // DMA instruction q (= wave*NDMA + i) fills rows [RPI*q, RPI*(q+1)) of an
+  // operand stage, 1 KiB contiguous: lane l lands at row RPI*q + l/SL,
+  // physical slot l%SL, so it fetches logical slot (l%SL) ^ swz(row).
+  uint32_t voffA[8], voffB[8];  // NDMA <= 8 used (fixed bound: see below)
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int row = lrow + 32 * i;
-    ldsw[i] = row * kRowBytes + ((lslot ^ swz8(row)) << 4);
+  for (int i = 0; i < NDMA; ++i) {
+    const int row = (wave * NDMA + i) * RPI + lane / SL;
+    const uint32_t slot = (uint32_t)((lane % SL) ^ slot_swz<ROWB>(row));
+    voffA[i] = (uint32_t)row * (uint32_t)lda_bytes + slot * 16u;
+    voffB[i] = (uint32_t)row * (uint32_t)ldb_bytes + slot * 16u;
   }
-  // fragment reads: A row m = wm*128 + 32*i + (lane&31), logical slot
-  // 4*(lane>>5) + s for K sub-step s.
+  // fragment reads: A row m = wm*128 + 32*i + (lane&31); half h = lane>>5
+  // owns logical slots [h*SUB, h*SUB + SUB), one per sub-step.
   int rdA[4], rdB[4], fxA[4], fxB[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int ma = wm * 128 + 32 * i + (lane & 31);
     const int nb = wn * 128 + 32 * i + (lane & 31);
-    rdA[i] = ma * kRowBytes;
-    rdB[i] = nb * kRowBytes;
-    fxA[i] = (4 * (lane >> 5)) ^ swz8(ma);
-    fxB[i] = (4 * (lane >> 5)) ^ swz8(nb);
+    rdA[i] = ma * ROWB;
+    rdB[i] = nb * ROWB;
+    fxA[i] = (SUB * (lane >> 5)) ^ slot_swz<ROWB>(ma);
+    fxB[i] = (SUB * (lane >> 5)) ^ slot_swz<ROWB>(nb);
   }
 
-  u32x4_t sa[8], sb[8];
-  auto gload = [&](int ks) {
+  // DMA of K step ks into `stage`; past the last step the offset is made
+  // out of range, so the hardware fills zeros without touching memory (the
+  // schedule stays branch-free; those stages are never read).
+  auto dma = [&](int ks, int stage) {
+    char* a = lds + stage * STB;
+    char* b = a + OPB;
+    const uint32_t k0 = ks < ks_end ? (uint32_t)ks * ROWB : 0x80000000u;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      // all offsets in the VGPR offset (soffset = 0) so the hardware range
-      // check sees the full offset and returns zeros past the operand's rows
-      const uint32_t ka = voffA + 32u * i * (uint32_t)lda_bytes + (uint32_t)ks * kRowBytes;
-      const uint32_t kb = voffB + 32u * i * (uint32_t)ldb_bytes + (uint32_t)ks * kRowBytes;
-      sa[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, (int)ka, 0, 0);
-      sb[i] = __builtin_amdgcn_raw_buffer_load_b128(rb, (int)kb, 0, 0);
+    for (int i = 0; i < NDMA; ++i) {
+      const int q = wave * NDMA + i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(a + q * 1024), 16,
+                                               voffA[i] + k0, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(b + q * 1024), 16,
+                                               voffB[i] + k0, 0, 0, 0);
     }
   };
-  auto lstore = [&](int stage) {
-    char* a = lds + stage * (2 * kStageBytes);
-    char* b = a + kStageBytes;
+  auto frag = [&](int stage, int s, u32x4_t (&fa)[4], u32x4_t (&fb)[4]) {
+    const char* a = lds + stage * STB;
+    const char* b = a + OPB;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      *reinterpret_cast<u32x4_t*>(a + ldsw[i]) = sa[i];
-      *reinterpret_cast<u32x4_t*>(b + ldsw[i]) = sb[i];
+    for (int i = 0; i < 4; ++i) {
+      fa[i] = *reinterpret_cast<const u32x4_t*>(a + rdA[i] + ((fxA[i] ^ s) << 4));
+      fb[i] = *reinterpret_cast<const u32x4_t*>(b + rdB[i] + ((fxB[i] ^ s) << 4));
     }
   };
-  auto compute = [&](int stage) {
-    const char* a = lds + stage * (2 * kStageBytes);
-    const char* b = a + kStageBytes;
+  auto mfma16 = [&](const u32x4_t (&fa)[4], const u32x4_t (&fb)[4]) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      u32x4_t fa[4], fb[4];
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
+  };
+
+  // Step j lives in stage j % S; S steps of DMA are always in flight. In
+  // step j, each of the first SUB-1 sub-steps issues the next sub-step's 8
+  // fragment reads interleaved with its 16 MFMAs. Then the wave waits for its
+  // reads and for step j+1's DMA, the barrier publishes every wave's DMA and
+  // retires stage j % S, and the last sub-step's 16 MFMAs run interleaved
+  // with the DMA of step j+S into that stage and the fragment reads of step
+  // j+1's sub-step 0. (Per-wave in-order LDS returns make lgkmcnt waits on
+  // the older reads exact.)
+#pragma unroll
+  for (int p = 0; p < S; ++p) dma(ks_begin + p, p);
+  KD_VMCNT((S - 1) * NI);
+  __syncthreads();
+  u32x4_t fa[2][4], fb[2][4];
+  frag(0, 0, fa[0], fb[0]);
+  int st = 0;
+  for (int j = 0; j < nsteps; ++j) {
+#pragma unroll
+    for (int s = 0; s < SUB - 1; ++s) {
+      frag(st, s + 1, fa[(s + 1) & 1], fb[(s + 1) & 1]);
+      mfma16(fa[s & 1], fb[s & 1]);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f & ~0x0f00);  // lgkmcnt(0)
+    KD_VMCNT((S - 2) * NI);
+    __syncthreads();
+    const int nst = st + 1 == S ? 0 : st + 1;
+    dma(ks_begin + j + S, st);
+    frag(nst, 0, fa[SUB & 1], fb[SUB & 1]);
+    mfma16(fa[(SUB - 1) & 1], fb[(SUB - 1) & 1]);
+#pragma unroll
+    for (int q = 0; q < 2 * NDMA; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (DMA)
+      if (q < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 16 - 2 * NDMA, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    st = nst;
+    if constexpr ((SUB & 1) != 0) {
+      // odd sub-step count: next step's sub-step 0 landed in buffer 1
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        fa[i] = *reinterpret_cast<const u32x4_t*>(a + rdA[i] + ((fxA[i] ^ s) << 4));
-        fb[i] = *reinterpret_cast<const u32x4_t*>(b + rdB[i] + ((fxB[i] ^ s) << 4));
+        fa[0][i] = fa[1][i];
+        fb[0][i] = fb[1][i];
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
     }
-  };
-
-  gload(ks_begin);
-  lstore(0);
-  __syncthreads();
-  for (int ks = ks_begin; ks < ks_end; ++ks) {
-    const int stage = (ks - ks_begin) & 1;
-    const bool more = ks + 1 < ks_end;
-    if (more) gload(ks + 1);
-    compute(stage);
-    if (more) lstore(stage ^ 1);
-    __syncthreads();
   }
+  KD_VMCNT(0);
+  __syncthreads();
 }
 
 // ---------------------------------------------------------------- wave ops --

@@ -12,6 +12,8 @@
 #include "kd_device.h"
 #include "kd_launch.h"
 
+#include <string.h>
+
 namespace kd {
 
 // ------------------------------------------------------------------ small --
@@ -96,8 +98,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
   const int ld = D * eb;
   const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
   AccTile acc;
-  gemm_tile<T>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
-               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowBytes,
+  gemm_tile<T, kRowB, kStages>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
+               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowB,
                lds, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -194,7 +196,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     const float* __restrict__ tp, int K, T* dZ, int64_t ldz, T* dZt, int64_t ldzt,
     float* part_C, int nVT) {
   constexpr int kStage = 128 * 256 * 4;  // 128 token rows x 256 vocab, fp32
-  __shared__ __attribute__((aligned(16))) char lds[kStage + 4 * 256 * 4];
+  constexpr int kEpi = kStage + 4 * 256 * 4;
+  __shared__ __attribute__((aligned(16))) char lds[kLdsMain > kEpi ? kLdsMain : kEpi];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
@@ -202,8 +205,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   const int ld = D * eb;
   const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
   AccTile acc;
-  gemm_tile<T>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
-               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowBytes,
+  gemm_tile<T, kRowB, kStages>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
+               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowB,
                lds, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -231,58 +234,104 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     }
     __syncthreads();
 
-    for (int rr = 0; rr < 32; ++rr) {
-      const int n = wave * 32 + rr;
-      const int tl = n0 + 128 * h + n;  // token row within the chunk
-      float* srow = st + n * 256;
-      const int myslot = lane ^ hsw16(n);
-      f32x4_t G = {0.f, 0.f, 0.f, 0.f};
-      if (tl < rows) {
-        const f32x4_t z = *reinterpret_cast<const f32x4_t*>(srow + myslot * 4);
-        const float cm = rowCoefM[tl], cf = rowCoef[tl], L2 = rowL2[tl];
+    // per-row scalars of this wave's 32 rows, lane rr holding row rr
+    const int tl_lane = n0 + 128 * h + wave * 32 + (lane & 31);
+    float my_cm = 0.f, my_cf = 0.f, my_l2 = 0.f;
+    if (tl_lane < rows) {
+      my_cm = rowCoefM[tl_lane];
+      my_cf = rowCoef[tl_lane];
+      my_l2 = rowL2[tl_lane];
+    }
+    for (int b16 = 0; b16 < 2; ++b16) {
+      // the first 128 teacher entries of 16 rows, loaded in one batch
+      int bi[16][2];
+      float bp[16][2];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ok = vfull || (m0 + vl0 + e < V);
-          G[e] = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
+      for (int rr = 0; rr < 16; ++rr) {
+        const int tl = n0 + 128 * h + wave * 32 + b16 * 16 + rr;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int k = 64 * e + lane;
+          const bool ok = tl < rows && k < K;
+          bi[rr][e] = ok ? tidx[(int64_t)tl * K + k] : -1;
+          bp[rr][e] = ok ? tp[(int64_t)tl * K + k] : 0.f;
         }
-        // teacher entries of this row inside [m0, m0 + 256)
-        *reinterpret_cast<f32x4_t*>(corr + vl0) = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        __builtin_amdgcn_wave_barrier();
-        float cpart = 0.f;
-        bool hit = false;
-        const int32_t* ir = tidx + (int64_t)tl * K;
-        const float* pr = tp + (int64_t)tl * K;
-        for (int kb = 0; kb < K; kb += 64) {
-          const int k = kb + lane;
-          if (k < K) {
-            const int dv = ir[k] - m0;
-            if (dv >= 0 && dv < kTile) {
-              const float pk = pr[k];
-              const float zv = srow[(((dv >> 2) ^ hsw16(n)) << 2) + (dv & 3)];
-              cpart += pk * zv;
-              corr[dv] = -cf * pk;
-              hit = true;
+      }
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int n = wave * 32 + b16 * 16 + rr;
+        const int tl = n0 + 128 * h + n;  // token row within the chunk
+        float* srow = st + n * 256;
+        const int myslot = lane ^ hsw16(n);
+        f32x4_t G = {0.f, 0.f, 0.f, 0.f};
+        if (tl < rows) {
+          const f32x4_t z = *reinterpret_cast<const f32x4_t*>(srow + myslot * 4);
+          const float cm = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cm), b16 * 16 + rr));
+          const float cf = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cf), b16 * 16 + rr));
+          const float L2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_l2), b16 * 16 + rr));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool ok = vfull || (m0 + vl0 + e < V);
+            G[e] = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
+          }
+          // teacher entries of this row inside [m0, m0 + 256): distinct
+          // indices, so each hit owns its column; corrections go through a
+          // zeroed per-wave row buffer to the lanes owning the columns
+          float cpart = 0.f;
+          bool hit = false;
+          int dv[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            dv[e] = bi[rr][e] - m0;
+            hit |= (unsigned)dv[e] < (unsigned)kTile;
+          }
+          bool hit_tail = false;
+          if (K > 128) {
+            for (int k = 128 + lane; k < K; k += 64) {
+              const int d2 = tidx[(int64_t)tl * K + k] - m0;
+              hit_tail |= (unsigned)d2 < (unsigned)kTile;
+            }
+          }
+          if (__any(hit || hit_tail)) {
+            *reinterpret_cast<f32x4_t*>(corr + vl0) = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+              if ((unsigned)dv[e] < (unsigned)kTile) {
+                const float zv = srow[(((dv[e] >> 2) ^ hsw16(n)) << 2) + (dv[e] & 3)];
+                cpart += bp[rr][e] * zv;
+                corr[dv[e]] = -cf * bp[rr][e];
+              }
+            }
+            if (K > 128) {
+              for (int k = 128 + lane; k < K; k += 64) {
+                const int d2 = tidx[(int64_t)tl * K + k] - m0;
+                if ((unsigned)d2 < (unsigned)kTile) {
+                  const float pk = tp[(int64_t)tl * K + k];
+                  const float zv = srow[(((d2 >> 2) ^ hsw16(n)) << 2) + (d2 & 3)];
+                  cpart += pk * zv;
+                  corr[d2] = -cf * pk;
+                }
+              }
+            }
+            __builtin_amdgcn_wave_barrier();
+            const f32x4_t c = *reinterpret_cast<const f32x4_t*>(corr + vl0);
+            G += c;
+            cpart = wave_sum(cpart);
+          }
+          if (lane == 0) part_C[(int64_t)tl * nVT + mt] = cpart;
+          if (dZ != nullptr) {
+            T* dst = dZ + (int64_t)tl * ldz + m0 + vl0;
+            if constexpr (sizeof(T) == 2) {
+              u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
+              *reinterpret_cast<u32x2_t*>(dst) = pk2;
+            } else {
+              *reinterpret_cast<f32x4_t*>(dst) = G;
             }
           }
         }
-        __builtin_amdgcn_wave_barrier();
-        if (__any(hit)) {
-          const f32x4_t c = *reinterpret_cast<const f32x4_t*>(corr + vl0);
-          G += c;
-          cpart = wave_sum(cpart);
-        }
-        if (lane == 0) part_C[(int64_t)tl * nVT + mt] = cpart;
-        if (dZ != nullptr) {
-          T* dst = dZ + (int64_t)tl * ldz + m0 + vl0;
-          if constexpr (sizeof(T) == 2) {
-            u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
-            *reinterpret_cast<u32x2_t*>(dst) = pk2;
-          } else {
-            *reinterpret_cast<f32x4_t*>(dst) = G;
-          }
-        }
+        if (dZt != nullptr) *reinterpret_cast<f32x4_t*>(srow + myslot * 4) = G;
       }
-      if (dZt != nullptr) *reinterpret_cast<f32x4_t*>(srow + myslot * 4) = G;
     }
     __syncthreads();
 
@@ -392,7 +441,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const int kb = sidx * per, ke = min(ks_total, kb + per);
   AccTile acc;
   const int mrows = min(kTile, rows - m0), nrows = min(kTile, D - n0);
-  gemm_tile<T>(make_rsrc(dZ + (int64_t)m0 * ldz, (uint32_t)(mrows * lda)), lda,
+  gemm_tile<T, kRowB, kStages>(make_rsrc(dZ + (int64_t)m0 * ldz, (uint32_t)(mrows * lda)), lda,
                make_rsrc(Wt + (int64_t)n0 * ldw, (uint32_t)(nrows * ldb)), ldb, kb, ke, lds, acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -442,26 +491,41 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZt, i
   const int lda = (int)(ldzt * eb), ldb = (int)(ldh * eb);
   const int mrows = min(kTile, V - m0), nrows = min(kTile, D - n0);
   AccTile acc;
-  gemm_tile<T>(make_rsrc(dZt + (int64_t)m0 * ldzt, (uint32_t)(mrows * lda)), lda,
+  gemm_tile<T, kRowB, kStages>(make_rsrc(dZt + (int64_t)m0 * ldzt, (uint32_t)(mrows * lda)), lda,
                make_rsrc(Hct + (int64_t)n0 * ldh, (uint32_t)(nrows * ldb)), ldb, 0, ks_total, lds,
                acc);
+  // fp32 read-modify-write of the output tile through a buffer resource over
+  // its rows (rows past V are out of range: loads give 0, stores are dropped);
+  // each 64-value block is loaded in one batch before it is stored, so the
+  // memory round trips overlap instead of serialising element by element.
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(gW + (int64_t)m0 * D, (uint32_t)mrows * D * 4u);
+  const uint32_t col0 = (uint32_t)(n0 + wn * 128 + (lane & 31));  // base is column 0
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
+    float old[4][16];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int d = n0 + wn * 128 + 32 * j + (lane & 31);
-      if (d >= D) continue;
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int v = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (v < V) {
-          float* o = gW + (int64_t)v * D + d;
-          *o = beta ? *o + acc.v[i][j][r] : acc.v[i][j][r];
-        }
+        const uint32_t row = (uint32_t)(wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
+        const uint32_t off = (row * (uint32_t)D + col0 + 32u * j) * 4u;
+        old[j][r] = 0.f;
+        if (beta && (int)col0 + 32 * j < D)
+          old[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, (int)off, 0, 0));
       }
-    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint32_t row = (uint32_t)(wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
+        const uint32_t off = (row * (uint32_t)D + col0 + 32u * j) * 4u;
+        if ((int)col0 + 32 * j < D)
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, old[j][r] + acc.v[i][j][r]),
+                                                ro, (int)off, 0, 0);
+      }
+  }
 }
 
 // ------------------------------------------------------------ index check --
@@ -486,7 +550,101 @@ __global__ void k_check_indices(const int32_t* idx, int64_t N, int K, int64_t V,
 // ================================================================ launchers ==
 using namespace kd;
 
+#include <atomic>
+#include <mutex>
+#include <vector>
+
+#include "../../include/kdtopk.h"
+
 static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// ------------------------------------------------- event instrumentation ----
+namespace {
+enum ProfKind {
+  P_COUNT_VALID, P_TRANSPOSE_W, P_PROLOGUE, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH,
+  P_DH_REDUCE, P_TRANSPOSE_HC, P_DW, P_FINALIZE, P_FILL, P_NKINDS
+};
+const char* const kProfNames[P_NKINDS] = {
+    "count_valid", "transpose_W", "teacher_prologue", "logits_lse", "lse_merge", "dz",
+    "row_loss", "dh", "dh_reduce", "transpose_Hc", "dw", "finalize_loss", "fill"};
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+  double flops;
+};
+std::atomic<bool> g_prof_on{false};
+std::mutex g_prof_mu;
+std::vector<ProfRec> g_prof_recs;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Records an event pair around the launches in its scope when enabled.
+struct ProfScope {
+  int kind;
+  double flops;
+  hipStream_t s;
+  hipEvent_t a = nullptr;
+  ProfScope(int k, double f, hipStream_t st) : kind(k), flops(f), s(st) {
+    if (!g_prof_on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> g(g_prof_mu);
+    a = prof_event();
+    if (a) (void)hipEventRecord(a, s);
+  }
+  ~ProfScope() {
+    if (!a) return;
+    std::lock_guard<std::mutex> g(g_prof_mu);
+    hipEvent_t b = prof_event();
+    if (!b) return;
+    (void)hipEventRecord(b, s);
+    g_prof_recs.push_back({kind, a, b, flops});
+  }
+};
+}  // namespace
+
+extern "C" kd_status kd_profile_enable(int on) {
+  g_prof_on.store(on != 0);
+  return KD_OK;
+}
+
+extern "C" int kd_profile_read(kd_kernel_time* out, int max) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  double ms[P_NKINDS] = {0}, fl[P_NKINDS] = {0};
+  int64_t n[P_NKINDS] = {0};
+  int rc = 0;
+  for (const ProfRec& r : g_prof_recs) {
+    float t = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&t, r.a, r.b) != hipSuccess)
+      rc = -1;
+    ms[r.kind] += t;
+    fl[r.kind] += r.flops;
+    n[r.kind] += 1;
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+  }
+  g_prof_recs.clear();
+  if (rc != 0) return rc;
+  int w = 0;
+  for (int k = 0; k < P_NKINDS && w < max; ++k) {
+    if (n[k] == 0) continue;
+    kd_kernel_time& o = out[w++];
+    memset(o.name, 0, sizeof(o.name));
+    strncpy(o.name, kProfNames[k], sizeof(o.name) - 1);
+    o.launches = n[k];
+    o.total_ms = ms[k];
+    o.flops = fl[k];
+  }
+  return w;
+}
 
 template <typename T>
 static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
@@ -494,45 +652,73 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
   const T* Hc = static_cast<const T*>(a.Hc);
   const int TMv = cdiv(a.V, kTile), TNt = cdiv(a.rows, kTile);
   const float k2 = kLog2e * a.inv_tau;
+  const double gemm_flops = 2.0 * (double)a.rows * (double)a.D * (double)a.V;
 
-  hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
+{
+    ProfScope ps_(P_PROLOGUE, 0.0, s);
+    hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
                      a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.inv_nvalid, a.p, a.rowM, a.rowH,
                      a.rowCoef, a.rowCoefM);
-  hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
+    }
+{
+    ProfScope ps_(P_LOGITS, gemm_flops, s);
+    hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
                      (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT);
-  hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
+    }
+{
+    ProfScope ps_(P_MERGE, 0.0, s);
+    hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
                      a.rows, a.nVT, a.rowL2);
-  hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
+    }
+{
+    ProfScope ps_(P_DZ, gemm_flops, s);
+    hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
                      a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.tidx, a.p, a.K,
                      static_cast<T*>(a.dZ), a.ldz, static_cast<T*>(a.dZt), a.ldzt, a.part_C,
                      a.nVT);
-  hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 256)), dim3(256), 0, s, a.part_C, a.nVT,
+    }
+{
+    ProfScope ps_(P_ROW_LOSS, 0.0, s);
+    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 256)), dim3(256), 0, s, a.part_C, a.nVT,
                      a.rowL2, a.rowM, a.rowH, a.rowCoef, a.rows, a.inv_tau, a.loss_per_token,
                      a.block_partial);
+    }
   if (a.gH != nullptr) {
     const int TM = cdiv(a.rows, kTile), TN = cdiv(a.D, kTile);
-    const int ks = (int)(a.ldz * sizeof(T) / kRowBytes);
+    const int ks = (int)(a.ldz * sizeof(T) / kRowB);
+{
+    ProfScope ps_(P_DH, gemm_flops, s);
     hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.dh_split), dim3(kThreads), 0, s,
                        static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.Wt), a.ldw,
                        a.rows, (int)a.D, TM, TN, ks, a.dh_split, static_cast<T*>(a.gH),
                        a.dh_partial);
+    }
     if (a.dh_split > 1) {
       const int64_t n = (int64_t)a.rows * a.D;
-      hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256),
+{
+    ProfScope ps_(P_DH_REDUCE, 0.0, s);
+    hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256),
                          0, s, a.dh_partial, a.dh_split, n, static_cast<T*>(a.gH));
+    }
     }
   }
   if (a.gW != nullptr) {
     // grid covers the padded extent so H_c^T's K padding is written as zeros
+{
+    ProfScope ps_(P_TRANSPOSE_HC, 0.0, s);
     hipLaunchKernelGGL(k_transpose_pad<T>, dim3(cdiv(a.ldh, 64), cdiv(a.D, 64)), dim3(256), 0,
                        s, Hc, (int64_t)a.rows, a.D, a.D, static_cast<T*>(a.Hct), a.ldh,
                        a.ldh);
+    }
     const int TM = cdiv(a.V, kTile), TN = cdiv(a.D, kTile);
     // K range = the chunk's token tiles (dZ^T columns past them are not written)
-    const int ks = (int)((int64_t)TNt * kTile * sizeof(T) / kRowBytes);
+    const int ks = (int)((int64_t)TNt * kTile * sizeof(T) / kRowB);
+{
+    ProfScope ps_(P_DW, gemm_flops, s);
     hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s,
                        static_cast<const T*>(a.dZt), a.ldzt, static_cast<const T*>(a.Hct), a.ldh,
                        (int)a.V, (int)a.D, TM, TN, ks, a.dw_beta, a.gW);
+    }
   }
   return (int)hipGetLastError();
 }
@@ -544,9 +730,13 @@ extern "C" int kd_launch_chunk(const KdChunkArgs* a, void* stream) {
 
 extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(256), 0, s, a->ignore, a->N, a->nvalid,
+{
+    ProfScope ps_(P_COUNT_VALID, 0.0, s);
+    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(256), 0, s, a->ignore, a->N, a->nvalid,
                      a->inv_nvalid);
+    }
   if (a->Wt != nullptr) {
+    ProfScope ps_(P_TRANSPOSE_W, 0.0, s);
     const dim3 grid(cdiv(a->ldw, 64), cdiv(a->D, 64));  // includes the zero padding
     if (a->dtype == 1)
       hipLaunchKernelGGL(k_transpose_pad<__bf16>, grid, dim3(256), 0, s,
@@ -559,8 +749,11 @@ extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
   }
   if (a->zero_gW != nullptr) {
     const int64_t n = a->V * a->D;
+{
+    ProfScope ps_(P_FILL, 0.0, s);
     hipLaunchKernelGGL(k_fill_f32, dim3(std::min<int64_t>(cdiv(n, 256), 16384)), dim3(256), 0, s,
                        a->zero_gW, n, 0.0f);
+    }
   }
   return (int)hipGetLastError();
 }
@@ -568,7 +761,10 @@ extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
 extern "C" int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid,
                                   float* loss, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipLaunchKernelGGL(k_finalize_loss, dim3(1), dim3(256), 0, s, partials, n, inv_nvalid, loss);
+{
+    ProfScope ps_(P_FINALIZE, 0.0, s);
+    hipLaunchKernelGGL(k_finalize_loss, dim3(1), dim3(256), 0, s, partials, n, inv_nvalid, loss);
+    }
   return (int)hipGetLastError();
 }
 
