@@ -1,0 +1,109 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark times (same chunk, same dtype, inputs from the same generators).
+
+The fp64 oracle cannot evaluate a full [N, V] batch in test time, so:
+  * 64 token rows sampled from the non-ignored rows (seed 1238) are checked
+    element by element -- their per-token loss and grad_hidden rows -- against
+    the oracle evaluated on those rows with the batch's N_valid as the mean's
+    divisor (rows are independent given N_valid);
+  * grad_W is checked on a separate call over a random 512-token sub-batch
+    (seed 1239) against the oracle's full [V, D] gradient of that sub-batch;
+  * properties that hold at any size: the loss equals the mean of the
+    per-token losses, ignored rows are exactly zero, sum_v grad_W[v, :] = 0
+    (Eq. 3 sums to zero over the vocabulary), and peak memory stays far below
+    the [N, V] logit tensor.
+"""
+import numpy as np
+import pytest
+import torch
+
+import kd_inputs as ki
+from oracle import kd_topk_kl
+from tests.helpers import TOL, rel_max, to64
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+WORKLOADS = ["loss4k", "loss32k", "packed", "long256k"]
+
+
+def _full_call(kd, w, inp):
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    out = kd.fwd_bwd(inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"],
+                     tau=w.tau, ignore=inp["ignore"], chunk=w.chunk, loss_per_token=True)
+    torch.cuda.synchronize()
+    peak_extra = torch.cuda.max_memory_allocated() - base
+    return out, peak_extra
+
+
+@pytest.mark.parametrize("name", WORKLOADS)
+def test_sampled_rows_and_properties(gpu_lib, name):
+    w = ki.WORKLOADS[name]
+    print(f"[scale] {name}: N={w.N} D={w.D} V={w.V} K={w.K} chunk={w.chunk} tau={w.tau}", flush=True)
+    inp = ki.make_workload_inputs(w, "cuda")
+    out, peak_extra = _full_call(gpu_lib, w, inp)
+    ign = inp["ignore"]
+    valid = torch.ones(w.N, dtype=torch.bool) if ign is None else (ign.cpu() == 0)
+    n_valid = int(valid.sum())
+    loss = float(out["loss"])
+    lpt = out["loss_per_token"].double().cpu()
+    assert np.isfinite(loss)
+    # loss = mean of the per-token losses over non-ignored rows
+    assert abs(loss - float(lpt.sum()) / n_valid) <= 1e-5 * abs(loss)
+    if ign is not None:
+        bad = (~valid).nonzero().flatten()[:32].to("cuda")
+        assert float(lpt[bad.cpu()].abs().max()) == 0.0
+        assert float(out["grad_hidden"].index_select(0, bad).float().abs().max()) == 0.0
+    # memory: inputs aside, the call holds its outputs and the workspace, whose
+    # vocabulary-sized part is bounded by one chunk -- never an [N, V] tensor
+    ws = gpu_lib.workspace_size(w.N, w.D, w.V, w.K, w.chunk, w.tau, gpu_lib.KD_BF16)
+    outputs = w.N * 4 + w.N * w.D * 2 + w.V * w.D * 4 + 4
+    assert peak_extra <= ws + outputs + (64 << 20), (peak_extra, ws, outputs)
+    if w.N >= 262144:
+        assert peak_extra < w.N * w.V * 2 / 4
+    # sum_v dL/dz_v = 0 (Eq. 3 with M = sum p), so every column of grad_W sums
+    # to zero up to the rounding of dZ to bf16: half-ulp errors of relative
+    # std ~2^-8/sqrt(3) give a column-sum noise of ~2.3e-3 times the column's
+    # 2-norm; 0.02 is ~9 sigma. A dropped term (e.g. the teacher correction)
+    # leaves a column sum of the order of the column norm itself.
+    gW = out["grad_W"].double()
+    colsum = (gW.sum(dim=0).abs() / gW.norm(dim=0).clamp_min(1e-30)).max().item()
+    assert colsum <= 0.02, colsum
+
+    rows = ki.sample_rows(valid.nonzero().flatten(), 64)
+    rows_d = rows.to("cuda")
+    h = to64(inp["hidden"].index_select(0, rows_d))
+    ref = kd_topk_kl(h, to64(inp["W"]), to64(inp["teacher_idx"].index_select(0, rows_d)),
+                     to64(inp["teacher_logit"].index_select(0, rows_d)), tau=w.tau,
+                     ignore=None, mean_denominator=n_valid, chunk=64)
+    e_l = rel_max(lpt[rows].numpy(), ref["loss_per_token"])
+    e_h = rel_max(to64(out["grad_hidden"].index_select(0, rows_d)), ref["grad_hidden"])
+    print(f"[scale] {name}: loss {loss:.6f}, sampled l_t rel {e_l:.2e}, grad_hidden rows "
+          f"{e_h:.2e}, sum_v grad_W {colsum:.2e}, peak extra {peak_extra / 2**30:.2f} GiB",
+          flush=True)
+    assert e_l <= TOL["bf16"]["loss"]
+    assert e_h <= TOL["bf16"]["grad"]
+
+
+@pytest.mark.parametrize("name", ["loss4k", "packed"])
+def test_grad_W_sub_batch(gpu_lib, name):
+    """grad_W of a 512-token sub-batch, every element against the oracle."""
+    w = ki.WORKLOADS[name]
+    inp = ki.make_workload_inputs(w, "cuda")
+    sel = ki.sub_batch(w.N, 512).to("cuda")
+    sub = {k: (v.index_select(0, sel).contiguous() if torch.is_tensor(v) and v.shape[0] == w.N
+               else v) for k, v in inp.items()}
+    out = gpu_lib.fwd_bwd(sub["hidden"], inp["W"], sub["teacher_idx"], sub["teacher_logit"],
+                          tau=w.tau, ignore=sub["ignore"], chunk=w.chunk, loss_per_token=True)
+    torch.cuda.synchronize()
+    ref = kd_topk_kl(to64(sub["hidden"]), to64(inp["W"]), to64(sub["teacher_idx"]),
+                     to64(sub["teacher_logit"]), tau=w.tau, ignore=to64(sub["ignore"]), chunk=256)
+    e_w = rel_max(to64(out["grad_W"]), ref["grad_W"])
+    e_h = rel_max(to64(out["grad_hidden"]), ref["grad_hidden"])
+    e_l = abs(float(out["loss"]) - ref["loss"]) / abs(ref["loss"])
+    print(f"[scale] {name} 512-token sub-batch: loss rel {e_l:.2e}, grad_hidden {e_h:.2e}, "
+          f"grad_W {e_w:.2e}", flush=True)
+    assert e_l <= TOL["bf16"]["loss"]
+    assert e_h <= TOL["bf16"]["grad"]
+    assert e_w <= TOL["bf16"]["grad"]
