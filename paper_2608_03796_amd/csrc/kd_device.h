@@ -21,9 +21,9 @@ typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
 typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2_t;
 
 constexpr int kTile = 256;                       // BM = BN
-constexpr int kThreads = 256;                    // 4 waves of 64, 2 x 2
-constexpr int kRowB = 64;                        // bytes of a tile row per K step
-constexpr int kStages = 5;                       // LDS stages of the main loop
+constexpr int kThreads = 512;                    // 8 waves of 64: 2 (M) x 4 (N)
+constexpr int kRowB = 128;                       // bytes of a tile row per K step
+constexpr int kStages = 2;                       // LDS stages of the main loop
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -64,31 +64,35 @@ struct Elt<float> {
   static constexpr int bytes = 4;
 };
 
-// MFMA step on one 16-byte K slot of A (rows m) and B (rows n). The K order
-// inside a slot only has to agree between A and B, which it does by
-// construction: both fragments come from the same logical slot.
-__device__ __forceinline__ f32x16_t mfma_slot(u32x4_t a, u32x4_t b, f32x16_t c, __bf16*) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+// MFMA step on one 16-byte K slot of A (rows m) and B (rows n), 16x16 output
+// block. The K order inside a slot only has to agree between A and B, which
+// it does by construction: both fragments come from the same logical slot.
+__device__ __forceinline__ f32x4_t mfma_slot(u32x4_t a, u32x4_t b, f32x4_t c, __bf16*) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
-__device__ __forceinline__ f32x16_t mfma_slot(u32x4_t a, u32x4_t b, f32x16_t c, float*) {
+__device__ __forceinline__ f32x4_t mfma_slot(u32x4_t a, u32x4_t b, f32x4_t c, float*) {
   f32x4_t fa = __builtin_bit_cast(f32x4_t, a);
   f32x4_t fb = __builtin_bit_cast(f32x4_t, b);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[0], fb[0], c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[1], fb[1], c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[2], fb[2], c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[3], fb[3], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[0], fb[0], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[1], fb[1], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[2], fb[2], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[3], fb[3], c, 0, 0, 0);
   return c;
 }
 
-// Accumulator layout of one wave (wm, wn) after gemm_tile: acc[i][j][r] is
-// C[m][n] with
-//   m = wm*128 + 32*i + 8*(r>>2) + 4*(lane>>5) + (r&3)
-//   n = wn*128 + 32*j + (lane&31)
-// (the 32x32 MFMA output layout: lane holds column lane&31, 4 groups of 4 rows).
+// Accumulator layout of wave w (wm = w >> 2 in 0..1, wn = w & 3 in 0..3)
+// after gemm_tile: acc.v[i][j][r] (i < 8, j < 4, r < 4) is C[m][n] with
+//   m = wm*128 + 16*i + 4*(lane>>4) + r
+//   n = wn*64 + 16*j + (lane&15)
+// (the 16x16 MFMA output layout: lane holds column lane&15 of 4 rows).
 struct AccTile {
-  f32x16_t v[4][4];
+  f32x4_t v[8][4];
 };
+__device__ __forceinline__ int acc_m(int wm, int i, int lane, int r) {
+  return wm * 128 + 16 * i + 4 * (lane >> 4) + r;
+}
+__device__ __forceinline__ int acc_n(int wn, int j, int lane) { return wn * 64 + 16 * j + (lane & 15); }
 
 // One 256x256 output tile: acc = A[m0:m0+256, k-range] * B[n0:n0+256, k-range]^T.
 //
@@ -122,15 +126,14 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
                                           __amdgpu_buffer_rsrc_t rb, int ldb_bytes, int ks_begin,
                                           int ks_end, char* lds, AccTile& acc) {
   constexpr int SL = ROWB / 16;           // 16-byte slots per row
-  constexpr int SUB = SL / 2;             // MFMA sub-steps per K step
+  constexpr int SUB = SL / 4;             // MFMA sub-steps (64-byte K slices) per K step
   constexpr int OPB = kTile * ROWB;       // one operand's stage
   constexpr int STB = 2 * OPB;            // one stage (A and B)
   constexpr int RPI = 1024 / ROWB;        // rows per 1 KiB DMA instruction
-  constexpr int NDMA = kTile / RPI / 4;   // DMA instructions per operand per wave
+  constexpr int NDMA = kTile / RPI / 8;   // DMA instructions per operand per wave
   constexpr int NI = 2 * NDMA;            // per K step per wave (vmcnt units)
   static_assert(SUB >= 2, "two or more sub-steps per K step");
   static_assert((S - 1) * NI <= 63, "vmcnt range of the in-flight DMA steps");
-  static_assert(2 * NDMA <= 16, "one MFMA per DMA instruction in the last sub-step");
   static_assert(NDMA <= 8, "DMA offsets array");
   // (arrays captured by the lambdas below have literal bounds: clang's host
   // pass rejects a second instantiation when the bound is a dependent local)
@@ -138,14 +141,12 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
 
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc.v[i][j][r] = 0.0f;
+    for (int j = 0; j < 4; ++j) acc.v[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nsteps = ks_end - ks_begin;
   if (nsteps <= 0) {
@@ -156,7 +157,7 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
   // DMA instruction q (= wave*NDMA + i) fills rows [RPI*q, RPI*(q+1)) of an
   // operand stage, 1 KiB contiguous: lane l lands at row RPI*q + l/SL,
   // physical slot l%SL, so it fetches logical slot (l%SL) ^ swz(row).
-  uint32_t voffA[8], voffB[8];  // NDMA <= 8 used (fixed bound: see below)
+  uint32_t voffA[8], voffB[8];  // NDMA <= 8 used (fixed bound: see above)
 #pragma unroll
   for (int i = 0; i < NDMA; ++i) {
     const int row = (wave * NDMA + i) * RPI + lane / SL;
@@ -164,17 +165,20 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
     voffA[i] = (uint32_t)row * (uint32_t)lda_bytes + slot * 16u;
     voffB[i] = (uint32_t)row * (uint32_t)ldb_bytes + slot * 16u;
   }
-  // fragment reads: A row m = wm*128 + 32*i + (lane&31); half h = lane>>5
-  // owns logical slots [h*SUB, h*SUB + SUB), one per sub-step.
-  int rdA[4], rdB[4], fxA[4], fxB[4];
+  // fragment reads: 16x16 blocks; lane group g = lane>>4 reads logical slot
+  // 4*s + g of row (block base + lane&15) in sub-step s.
+  int rdA[8], fxA[8], rdB[4], fxB[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ma = wm * 128 + 32 * i + (lane & 31);
-    const int nb = wn * 128 + 32 * i + (lane & 31);
+  for (int i = 0; i < 8; ++i) {
+    const int ma = wm * 128 + 16 * i + (lane & 15);
     rdA[i] = ma * ROWB;
-    rdB[i] = nb * ROWB;
-    fxA[i] = (SUB * (lane >> 5)) ^ slot_swz<ROWB>(ma);
-    fxB[i] = (SUB * (lane >> 5)) ^ slot_swz<ROWB>(nb);
+    fxA[i] = (lane >> 4) ^ slot_swz<ROWB>(ma);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int nb = wn * 64 + 16 * j + (lane & 15);
+    rdB[j] = nb * ROWB;
+    fxB[j] = (lane >> 4) ^ slot_swz<ROWB>(nb);
   }
 
   // DMA of K step ks into `stage`; past the last step the offset is made
@@ -193,46 +197,46 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
                                                voffB[i] + k0, 0, 0, 0);
     }
   };
-  auto frag = [&](int stage, int s, u32x4_t (&fa)[4], u32x4_t (&fb)[4]) {
+  auto frag = [&](int stage, int s, u32x4_t (&fa)[8], u32x4_t (&fb)[4]) {
     const char* a = lds + stage * STB;
     const char* b = a + OPB;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa[i] = *reinterpret_cast<const u32x4_t*>(a + rdA[i] + ((fxA[i] ^ s) << 4));
-      fb[i] = *reinterpret_cast<const u32x4_t*>(b + rdB[i] + ((fxB[i] ^ s) << 4));
-    }
-  };
-  auto mfma16 = [&](const u32x4_t (&fa)[4], const u32x4_t (&fb)[4]) {
+    for (int i = 0; i < 8; ++i)
+      fa[i] = *reinterpret_cast<const u32x4_t*>(a + rdA[i] + ((fxA[i] ^ (4 * s)) << 4));
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < 4; ++j)
+      fb[j] = *reinterpret_cast<const u32x4_t*>(b + rdB[j] + ((fxB[j] ^ (4 * s)) << 4));
+  };
+  auto mfma32 = [&](const u32x4_t (&fa)[8], const u32x4_t (&fb)[4]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
   };
 
   // Step j lives in stage j % S; S steps of DMA are always in flight. In
-  // step j, each of the first SUB-1 sub-steps issues the next sub-step's 8
-  // fragment reads interleaved with its 16 MFMAs. Then the wave waits for its
+  // step j, each of the first SUB-1 sub-steps issues the next sub-step's 12
+  // fragment reads interleaved with its 32 MFMAs. Then the wave waits for its
   // reads and for step j+1's DMA, the barrier publishes every wave's DMA and
-  // retires stage j % S, and the last sub-step's 16 MFMAs run interleaved
-  // with the DMA of step j+S into that stage and the fragment reads of step
-  // j+1's sub-step 0. (Per-wave in-order LDS returns make lgkmcnt waits on
-  // the older reads exact.)
+  // retires stage j % S, and the last sub-step's MFMAs run interleaved with
+  // the DMA of step j+S into that stage and the fragment reads of step j+1's
+  // sub-step 0. Two waves per SIMD fill each other's waits.
 #pragma unroll
   for (int p = 0; p < S; ++p) dma(ks_begin + p, p);
   KD_VMCNT((S - 1) * NI);
   __syncthreads();
-  u32x4_t fa[2][4], fb[2][4];
+  u32x4_t fa[2][8], fb[2][4];
   frag(0, 0, fa[0], fb[0]);
   int st = 0;
   for (int j = 0; j < nsteps; ++j) {
 #pragma unroll
     for (int s = 0; s < SUB - 1; ++s) {
       frag(st, s + 1, fa[(s + 1) & 1], fb[(s + 1) & 1]);
-      mfma16(fa[s & 1], fb[s & 1]);
+      mfma32(fa[s & 1], fb[s & 1]);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      for (int q = 0; q < 12; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
@@ -244,23 +248,22 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
     const int nst = st + 1 == S ? 0 : st + 1;
     dma(ks_begin + j + S, st);
     frag(nst, 0, fa[SUB & 1], fb[SUB & 1]);
-    mfma16(fa[(SUB - 1) & 1], fb[(SUB - 1) & 1]);
+    mfma32(fa[(SUB - 1) & 1], fb[(SUB - 1) & 1]);
 #pragma unroll
-    for (int q = 0; q < 2 * NDMA; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (DMA)
-      if (q < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    for (int q = 0; q < 12; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+      if (q < NI) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (DMA)
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 16 - 2 * NDMA, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
     st = nst;
     if constexpr ((SUB & 1) != 0) {
       // odd sub-step count: next step's sub-step 0 landed in buffer 1
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        fa[0][i] = fa[1][i];
-        fb[0][i] = fb[1][i];
-      }
+      for (int i = 0; i < 8; ++i) fa[0][i] = fa[1][i];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fb[0][i] = fb[1][i];
     }
   }
   KD_VMCNT(0);

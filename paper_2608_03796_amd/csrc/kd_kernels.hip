@@ -79,10 +79,10 @@ __global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, i
 }
 
 // ------------------------------------------------- logits + online LSE -----
-// Tile of z^T = W H_c^T (M = vocabulary, N = chunk tokens). Each lane holds 64
+// Tile of z^T = W H_c^T (M = vocabulary, N = chunk tokens). Each lane holds 32
 // vocabulary values of 4 tokens; the per-token max and sum of 2^(y - max) of
-// y = z log2(e)/tau are reduced in registers, across the two half-waves, and
-// across the two waves sharing the tokens through LDS. Output per (token,
+// y = z log2(e)/tau are reduced in registers, across the four lane groups of
+// the wave, and across the two waves sharing the tokens through LDS. Output per (token,
 // vocabulary tile): (max, sum) in base-2 units.
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict__ W,
@@ -103,49 +103,52 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
                lds, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const bool full = m0 + kTile <= V;
-  float* xch = reinterpret_cast<float*>(lds);
+  float* xch = reinterpret_cast<float*>(lds);  // [wn][j][16 lanes][max, sum]
   float rm[4], rs[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int v = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < 4; ++r) {
+        const int v = m0 + acc_m(wm, i, lane, r);
         const float y = acc.v[i][j][r] * k2;
         if (full || v < V) mx = fmaxf(mx, y);
       }
+    // the four lane groups (lane>>4) hold the other rows of the same token
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     float s = 0.f;
     if (mx != -INFINITY) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        for (int r = 0; r < 4; ++r) {
+          const int v = m0 + acc_m(wm, i, lane, r);
           const float e = fast_exp2(acc.v[i][j][r] * k2 - mx);
           if (full || v < V) s += e;
         }
     }
+    s += __shfl_xor(s, 16);
     s += __shfl_xor(s, 32);
     rm[j] = mx;
     rs[j] = s;
-    if (wm == 1 && lane < 32) {
-      xch[((wn * 4 + j) * 32 + lane) * 2 + 0] = mx;
-      xch[((wn * 4 + j) * 32 + lane) * 2 + 1] = s;
+    if (wm == 1 && lane < 16) {
+      xch[((wn * 4 + j) * 16 + lane) * 2 + 0] = mx;
+      xch[((wn * 4 + j) * 16 + lane) * 2 + 1] = s;
     }
   }
   __syncthreads();
-  if (wm == 0 && lane < 32) {
+  if (wm == 0 && lane < 16) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int t = n0 + wn * 128 + 32 * j + lane;
+      const int t = n0 + acc_n(wn, j, lane);
       const float m1 = rm[j], s1 = rs[j];
-      const float m2 = xch[((wn * 4 + j) * 32 + lane) * 2 + 0];
-      const float s2 = xch[((wn * 4 + j) * 32 + lane) * 2 + 1];
+      const float m2 = xch[((wn * 4 + j) * 16 + lane) * 2 + 0];
+      const float s2 = xch[((wn * 4 + j) * 16 + lane) * 2 + 1];
       const float mm = fmaxf(m1, m2);
       float ss = 0.f;
       if (mm != -INFINITY) ss = s1 * fast_exp2(m1 - mm) + s2 * fast_exp2(m2 - mm);
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     const float* __restrict__ tp, int K, T* dZ, int64_t ldz, T* dZt, int64_t ldzt,
     float* part_C, int nVT) {
   constexpr int kStage = 128 * 256 * 4;  // 128 token rows x 256 vocab, fp32
-  constexpr int kEpi = kStage + 4 * 256 * 4;
+  constexpr int kEpi = kStage + 8 * 256 * 4;  // staging + per-wave row buffers
   __shared__ __attribute__((aligned(16))) char lds[kLdsMain > kEpi ? kLdsMain : kEpi];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
@@ -210,45 +213,41 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
                lds, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   float* st = reinterpret_cast<float*>(lds);
   float* corr = reinterpret_cast<float*>(lds + kStage) + wave * 256;
   const int vl0 = 4 * lane;  // this lane's 4 vocabulary columns in the row pass
   const bool vfull = m0 + kTile <= V;
 
   for (int h = 0; h < 2; ++h) {
-    if (wn == h) {
+    if ((wn >> 1) == h) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int rq = 0; rq < 4; ++rq) {
-            const int n = 32 * j + (lane & 31);
-            const int vl = wm * 128 + 32 * i + 8 * rq + 4 * (lane >> 5);
-            const int slot = (vl >> 2) ^ hsw16(n);
-            f32x4_t x = {acc.v[i][j][4 * rq + 0], acc.v[i][j][4 * rq + 1],
-                         acc.v[i][j][4 * rq + 2], acc.v[i][j][4 * rq + 3]};
-            *reinterpret_cast<f32x4_t*>(st + n * 256 + slot * 4) = x;
-          }
+        for (int j = 0; j < 4; ++j) {
+          const int n = (wn & 1) * 64 + 16 * j + (lane & 15);  // token row of the half
+          const int vl = acc_m(wm, i, lane, 0);                 // 4 consecutive vocab
+          const int slot = (vl >> 2) ^ hsw16(n);
+          *reinterpret_cast<f32x4_t*>(st + n * 256 + slot * 4) = acc.v[i][j];
+        }
     }
     __syncthreads();
 
-    // per-row scalars of this wave's 32 rows, lane rr holding row rr
-    const int tl_lane = n0 + 128 * h + wave * 32 + (lane & 31);
+    // per-row scalars of this wave's 16 rows, lane rr holding row rr
+    const int tl_lane = n0 + 128 * h + wave * 16 + (lane & 15);
     float my_cm = 0.f, my_cf = 0.f, my_l2 = 0.f;
     if (tl_lane < rows) {
       my_cm = rowCoefM[tl_lane];
       my_cf = rowCoef[tl_lane];
       my_l2 = rowL2[tl_lane];
     }
-    for (int b16 = 0; b16 < 2; ++b16) {
-      // the first 128 teacher entries of 16 rows, loaded in one batch
-      int bi[16][2];
-      float bp[16][2];
+    for (int b8 = 0; b8 < 2; ++b8) {
+      // the first 128 teacher entries of 8 rows, loaded in one batch
+      int bi[8][2];
+      float bp[8][2];
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int tl = n0 + 128 * h + wave * 32 + b16 * 16 + rr;
+      for (int rr = 0; rr < 8; ++rr) {
+        const int tl = n0 + 128 * h + wave * 16 + b8 * 8 + rr;
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
           const int k = 64 * e + lane;
@@ -258,17 +257,18 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
         }
       }
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int n = wave * 32 + b16 * 16 + rr;
+      for (int rr = 0; rr < 8; ++rr) {
+        const int n = wave * 16 + b8 * 8 + rr;
         const int tl = n0 + 128 * h + n;  // token row within the chunk
         float* srow = st + n * 256;
         const int myslot = lane ^ hsw16(n);
         f32x4_t G = {0.f, 0.f, 0.f, 0.f};
         if (tl < rows) {
           const f32x4_t z = *reinterpret_cast<const f32x4_t*>(srow + myslot * 4);
-          const float cm = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cm), b16 * 16 + rr));
-          const float cf = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cf), b16 * 16 + rr));
-          const float L2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_l2), b16 * 16 + rr));
+          const int src = b8 * 8 + rr;
+          const float cm = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cm), src));
+          const float cf = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cf), src));
+          const float L2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_l2), src));
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const bool ok = vfull || (m0 + vl0 + e < V);
@@ -339,8 +339,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
       // column-major store: lane -> (vocab column, 8 consecutive tokens)
       const int q = lane & 15;
 #pragma unroll 4
-      for (int it = 0; it < 16; ++it) {
-        const int vl = it * 16 + wave * 4 + (lane >> 4);
+      for (int it = 0; it < 8; ++it) {
+        const int vl = it * 32 + wave * 4 + (lane >> 4);
         float x[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -444,16 +444,16 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   gemm_tile<T, kRowB, kStages>(make_rsrc(dZ + (int64_t)m0 * ldz, (uint32_t)(mrows * lda)), lda,
                make_rsrc(Wt + (int64_t)n0 * ldw, (uint32_t)(nrows * ldb)), ldb, kb, ke, lds, acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int j = 0; j < 4; ++j) {
+    const int d = n0 + acc_n(wn, j, lane);
+    if (d >= D) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int d = n0 + wn * 128 + 32 * j + (lane & 31);
-      if (d >= D) continue;
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int t = m0 + wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < 4; ++r) {
+        const int t = m0 + acc_m(wm, i, lane, r);
         if (t < rows) {
           if (split == 1)
             gH[(int64_t)t * D + d] = (T)acc.v[i][j][r];
@@ -461,7 +461,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
             partial[((int64_t)sidx * rows + t) * D + d] = acc.v[i][j][r];
         }
       }
-    }
+  }
 }
 
 template <typename T>
@@ -499,32 +499,37 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZt, i
   // each 64-value block is loaded in one batch before it is stored, so the
   // memory round trips overlap instead of serialising element by element.
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(gW + (int64_t)m0 * D, (uint32_t)mrows * D * 4u);
-  const uint32_t col0 = (uint32_t)(n0 + wn * 128 + (lane & 31));  // base is column 0
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float old[4][16];
+  for (int ib = 0; ib < 8; ib += 2) {
+    float old[2][4][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int di = 0; di < 2; ++di)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const uint32_t row = (uint32_t)(wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
-        const uint32_t off = (row * (uint32_t)D + col0 + 32u * j) * 4u;
-        old[j][r] = 0.f;
-        if (beta && (int)col0 + 32 * j < D)
-          old[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, (int)off, 0, 0));
-      }
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t row = (uint32_t)acc_m(wm, ib + di, lane, r);
+          const uint32_t col = (uint32_t)(n0 + acc_n(wn, j, lane));  // base is column 0
+          old[di][j][r] = 0.f;
+          if (beta && (int)col < D)
+            old[di][j][r] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(ro, (int)((row * (uint32_t)D + col) * 4u), 0, 0));
+        }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const uint32_t row = (uint32_t)(wm * 128 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3));
-        const uint32_t off = (row * (uint32_t)D + col0 + 32u * j) * 4u;
-        if ((int)col0 + 32 * j < D)
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, old[j][r] + acc.v[i][j][r]),
-                                                ro, (int)off, 0, 0);
-      }
+    for (int di = 0; di < 2; ++di)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t row = (uint32_t)acc_m(wm, ib + di, lane, r);
+          const uint32_t col = (uint32_t)(n0 + acc_n(wn, j, lane));
+          if ((int)col < D)
+            __builtin_amdgcn_raw_buffer_store_b32(
+                __builtin_bit_cast(uint32_t, old[di][j][r] + acc.v[ib + di][j][r]), ro,
+                (int)((row * (uint32_t)D + col) * 4u), 0, 0);
+        }
   }
 }
 
