@@ -30,7 +30,8 @@ struct Plan {
   int64_t Vp;          // V rounded up to the 256-column tile
   int64_t nVT;         // vocabulary tiles
   int64_t nchunks;
-  int64_t nblk;        // loss partials of a full chunk
+  int64_t nblk;        // loss partials of a full chunk (one per 64 rows)
+  int64_t G;           // chunks whose dZ^T is gathered before one dW GEMM
   int dh_split;
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_pc, off_lossp, off_dz, off_dzt, off_wt,
       off_hct, off_dhs, total;
@@ -78,7 +79,10 @@ Plan make_plan(const kd_problem* p) {
   pl.Vp = rup(pl.V, kTile);
   pl.nVT = pl.Vp / kTile;
   pl.nchunks = cdiv(pl.N, pl.c);
-  pl.nblk = cdiv(pl.c, kTile);
+  pl.nblk = cdiv(pl.c, 64);
+  // dW is accumulated in fp32 in place: each dW GEMM reads and writes all of
+  // grad_W once, so gather the dZ^T of up to ~8192 tokens per GEMM
+  pl.G = std::max<int64_t>(1, std::min<int64_t>(8192 / pl.cp, std::max<int64_t>(pl.nchunks, 1)));
   const int64_t dh_tiles = cdiv(pl.c, kTile) * cdiv(pl.D, kTile);
   pl.dh_split = choose_dh_split(dh_tiles, pl.Vp * pl.eb / 128);
   size_t t = 0;
@@ -95,9 +99,9 @@ Plan make_plan(const kd_problem* p) {
   pl.off_pc = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
   pl.off_dz = take((size_t)pl.cp * pl.Vp * pl.eb);
-  pl.off_dzt = take((size_t)pl.Vp * pl.cp * pl.eb);
+  pl.off_dzt = take((size_t)pl.Vp * pl.G * pl.cp * pl.eb);
   pl.off_wt = take((size_t)pl.D * pl.Vp * pl.eb);
-  pl.off_hct = take((size_t)pl.D * pl.cp * pl.eb);
+  pl.off_hct = take((size_t)pl.D * pl.G * pl.cp * pl.eb);
   pl.off_dhs = pl.dh_split > 1 ? take((size_t)pl.dh_split * pl.c * pl.D * 4) : 0;
   pl.total = align256(t);
   return pl;
@@ -174,6 +178,8 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
 
   float* rows = reinterpret_cast<float*>(ws + pl.off_rows);
   int64_t n_partials = 0;
+  int64_t group_tokens = 0;
+  bool dw_done = false;
   for (int64_t ci = 0; ci < pl.nchunks; ++ci) {
     const int64_t row0 = ci * pl.c;
     const int rcount = (int)std::min<int64_t>(pl.c, pl.N - row0);
@@ -203,10 +209,12 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     a.nVT = (int)pl.nVT;
     a.dZ = want_dh ? ws + pl.off_dz : nullptr;
     a.ldz = pl.Vp;
-    a.dZt = want_dw ? ws + pl.off_dzt : nullptr;
-    a.ldzt = pl.cp;
-    a.Hct = want_dw ? ws + pl.off_hct : nullptr;
-    a.ldh = pl.cp;
+    const int64_t slot = ci % pl.G;
+    a.dZt = want_dw ? ws + pl.off_dzt + slot * pl.cp * pl.eb : nullptr;
+    a.ldzt = pl.G * pl.cp;
+    a.Hct = want_dw ? ws + pl.off_hct + slot * pl.cp * pl.eb : nullptr;
+    a.ldh = pl.G * pl.cp;
+    a.cp = pl.cp;
     a.Wt = ws + pl.off_wt;
     a.ldw = pl.Vp;
     a.dh_split = pl.dh_split;
@@ -214,10 +222,26 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     a.loss_per_token = loss_per_token ? loss_per_token + row0 : nullptr;
     a.block_partial = lossp + n_partials;
     a.gH = want_dh ? static_cast<char*>(grad_hidden) + row0 * pl.D * pl.eb : nullptr;
-    a.gW = want_dw ? grad_W : nullptr;
-    a.dw_beta = (ci > 0 || accumulate_grad_W) ? 1 : 0;
     if (kd_launch_chunk(&a, hip_stream) != 0) return KD_ERR_DEVICE;
-    n_partials += cdiv(rcount, kTile);
+    n_partials += cdiv(rcount, 64);
+    group_tokens += rcount;
+    if (want_dw && (slot == pl.G - 1 || ci == pl.nchunks - 1)) {
+      KdDwArgs d{};
+      d.dtype = p->dtype;
+      d.D = pl.D;
+      d.V = pl.V;
+      d.dZt = ws + pl.off_dzt;
+      d.ldzt = pl.G * pl.cp;
+      d.Hct = ws + pl.off_hct;
+      d.ldh = pl.G * pl.cp;
+      d.kcols = slot * pl.cp + cdiv(rcount, kTile) * kTile;
+      d.tokens = group_tokens;
+      d.beta = (dw_done || accumulate_grad_W) ? 1 : 0;
+      d.gW = grad_W;
+      if (kd_launch_dw(&d, hip_stream) != 0) return KD_ERR_DEVICE;
+      dw_done = true;
+      group_tokens = 0;
+    }
   }
   if (kd_launch_finalize(lossp, (int)n_partials, inv_nvalid, loss, hip_stream) != 0)
     return KD_ERR_DEVICE;

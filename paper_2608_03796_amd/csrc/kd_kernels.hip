@@ -367,11 +367,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
 __global__ void k_row_loss(const float* part_C, int nVT, const float* rowL2, const float* rowM,
                            const float* rowH, const float* rowCoef, int rows, float inv_tau,
                            float* loss_per_token, float* block_partial) {
+  // 64 rows per block (16 per wave); one fixed-order partial per block
   __shared__ float red[4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float acc = 0.f;
-  for (int rr = 0; rr < 64; ++rr) {
-    const int r = blockIdx.x * 256 + wave * 64 + rr;
+  for (int rr = 0; rr < 16; ++rr) {
+    const int r = blockIdx.x * 64 + wave * 16 + rr;
     if (r >= rows) break;
     const float* pc = part_C + (int64_t)r * nVT;
     float c = 0.f;
@@ -684,7 +685,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     }
 {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
-    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 256)), dim3(256), 0, s, a.part_C, a.nVT,
+    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 64)), dim3(256), 0, s, a.part_C, a.nVT,
                      a.rowL2, a.rowM, a.rowH, a.rowCoef, a.rows, a.inv_tau, a.loss_per_token,
                      a.block_partial);
     }
@@ -707,23 +708,11 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     }
     }
   }
-  if (a.gW != nullptr) {
-    // grid covers the padded extent so H_c^T's K padding is written as zeros
-{
+  if (a.Hct != nullptr) {
+    // grid covers the chunk's padded column slot so H_c^T's K padding is zero
     ProfScope ps_(P_TRANSPOSE_HC, 0.0, s);
-    hipLaunchKernelGGL(k_transpose_pad<T>, dim3(cdiv(a.ldh, 64), cdiv(a.D, 64)), dim3(256), 0,
-                       s, Hc, (int64_t)a.rows, a.D, a.D, static_cast<T*>(a.Hct), a.ldh,
-                       a.ldh);
-    }
-    const int TM = cdiv(a.V, kTile), TN = cdiv(a.D, kTile);
-    // K range = the chunk's token tiles (dZ^T columns past them are not written)
-    const int ks = (int)((int64_t)TNt * kTile * sizeof(T) / kRowB);
-{
-    ProfScope ps_(P_DW, gemm_flops, s);
-    hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s,
-                       static_cast<const T*>(a.dZt), a.ldzt, static_cast<const T*>(a.Hct), a.ldh,
-                       (int)a.V, (int)a.D, TM, TN, ks, a.dw_beta, a.gW);
-    }
+    hipLaunchKernelGGL(k_transpose_pad<T>, dim3(cdiv(a.cp, 64), cdiv(a.D, 64)), dim3(256), 0, s,
+                       Hc, (int64_t)a.rows, a.D, a.D, static_cast<T*>(a.Hct), a.ldh, a.cp);
   }
   return (int)hipGetLastError();
 }
@@ -731,6 +720,22 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
 extern "C" int kd_launch_chunk(const KdChunkArgs* a, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   return a->dtype == 1 ? launch_chunk_impl<__bf16>(*a, s) : launch_chunk_impl<float>(*a, s);
+}
+
+template <typename T>
+static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
+  const int TM = cdiv(a.V, kTile), TN = cdiv(a.D, kTile);
+  const int ks = (int)(a.kcols * (int64_t)sizeof(T) / kRowB);
+  ProfScope ps_(P_DW, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
+  hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s, static_cast<const T*>(a.dZt),
+                     a.ldzt, static_cast<const T*>(a.Hct), a.ldh, (int)a.V, (int)a.D, TM, TN, ks,
+                     a.beta, a.gW);
+  return (int)hipGetLastError();
+}
+
+extern "C" int kd_launch_dw(const KdDwArgs* a, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return a->dtype == 1 ? launch_dw_impl<__bf16>(*a, s) : launch_dw_impl<float>(*a, s);
 }
 
 extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {

@@ -37,25 +37,39 @@ struct KdChunkArgs {
   int nVT;
   void* dZ;                 // [cp, ldz] or null (no dH)
   int64_t ldz;              // = padded vocabulary
-  void* dZt;                // [ldz, ldzt] or null (no dW)
-  int64_t ldzt;             // = padded chunk
-  void* Hct;                // [D, ldh] or null (no dW)
-  int64_t ldh;              // = padded chunk
+  void* dZt;                // this chunk's column slot of dZ^T [ldz, ldzt], or null
+  int64_t ldzt;             // = chunks per dW group * padded chunk
+  void* Hct;                // this chunk's column slot of H^T [D, ldh], or null
+  int64_t ldh;              // = ldzt
+  int64_t cp;               // padded chunk (width of a column slot)
   const void* Wt;           // [D, ldw] (dH)
   int64_t ldw;
   int dh_split;
   float* dh_partial;        // [dh_split, rows, D] when dh_split > 1
   // outputs
   float* loss_per_token;    // + row0, or null
-  float* block_partial;     // this chunk's cdiv(rows, 256) partial sums
+  float* block_partial;     // this chunk's cdiv(rows, 64) partial sums
   void* gH;                 // grad_hidden + row0 * D, or null
-  float* gW;                // grad_W or null
-  int dw_beta;              // 0 overwrite, 1 accumulate
+};
+
+// dW GEMM over the chunks of one group: grad_W (+)= dZ^T[:, :kcols] H^T[:, :kcols]^T
+struct KdDwArgs {
+  int dtype;
+  int64_t D, V;
+  const void* dZt;          // [Vp, ldzt]
+  int64_t ldzt;
+  const void* Hct;          // [D, ldh]
+  int64_t ldh;
+  int64_t kcols;            // columns of the group holding data (multiple of 256)
+  int64_t tokens;           // tokens in the group (for the FLOP count)
+  int beta;                 // 0 overwrite, 1 accumulate
+  float* gW;
 };
 
 extern "C" {
 int kd_launch_prepare(const KdPrepareArgs* a, void* stream);
 int kd_launch_chunk(const KdChunkArgs* a, void* stream);
+int kd_launch_dw(const KdDwArgs* a, void* stream);
 int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid, float* loss,
                        void* stream);
 int kd_launch_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag,
