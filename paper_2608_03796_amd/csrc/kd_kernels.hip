@@ -199,7 +199,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     const float* __restrict__ tp, int K, T* dZ, int64_t ldz, T* dZt, int64_t ldzt,
     float* part_C, int nVT) {
   constexpr int kStage = 128 * 256 * 4;  // 128 token rows x 256 vocab, fp32
-  constexpr int kEpi = kStage + 8 * 256 * 4;  // staging + per-wave row buffers
+  constexpr int kEpi = kStage;
   __shared__ __attribute__((aligned(16))) char lds[kLdsMain > kEpi ? kLdsMain : kEpi];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
@@ -215,7 +215,6 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 2, wn = wave & 3;
   float* st = reinterpret_cast<float*>(lds);
-  float* corr = reinterpret_cast<float*>(lds + kStage) + wave * 256;
   const int vl0 = 4 * lane;  // this lane's 4 vocabulary columns in the row pass
   const bool vfull = m0 + kTile <= V;
 
@@ -274,50 +273,49 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
             const bool ok = vfull || (m0 + vl0 + e < V);
             G[e] = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
           }
-          // teacher entries of this row inside [m0, m0 + 256): distinct
-          // indices, so each hit owns its column; corrections go through a
-          // zeroed per-wave row buffer to the lanes owning the columns
+          // Teacher entries of this row inside [m0, m0 + 256) (distinct indices,
+          // each ~0.2 per row per tile): a ballot over the lanes holding entries,
+          // then a scalar loop over the hits in lane order. Column dv lives in
+          // lane dv/4, component dv%4: that lane subtracts (g/tau) p, and the
+          // row's C partial sum_hits p * z is formed from z read across lanes.
           float cpart = 0.f;
-          bool hit = false;
-          int dv[2];
 #pragma unroll
           for (int e = 0; e < 2; ++e) {
-            dv[e] = bi[rr][e] - m0;
-            hit |= (unsigned)dv[e] < (unsigned)kTile;
-          }
-          bool hit_tail = false;
-          if (K > 128) {
-            for (int k = 128 + lane; k < K; k += 64) {
-              const int d2 = tidx[(int64_t)tl * K + k] - m0;
-              hit_tail |= (unsigned)d2 < (unsigned)kTile;
+            const int dv = bi[rr][e] - m0;
+            uint64_t mask = __ballot((unsigned)dv < (unsigned)kTile);
+            while (mask) {
+              const int src = __builtin_ctzll(mask);
+              mask &= mask - 1;
+              const int dvh = __builtin_amdgcn_readlane(dv, src);
+              const float ph = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bp[rr][e]), src));
+              const int owner = dvh >> 2, comp = dvh & 3;
+              const float zc = comp == 0 ? z[0] : comp == 1 ? z[1] : comp == 2 ? z[2] : z[3];
+              cpart += ph * __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, zc), owner));
+              const float d = lane == owner ? cf * ph : 0.f;
+              if (comp == 0) G[0] -= d;
+              else if (comp == 1) G[1] -= d;
+              else if (comp == 2) G[2] -= d;
+              else G[3] -= d;
             }
           }
-          if (__any(hit || hit_tail)) {
-            *reinterpret_cast<f32x4_t*>(corr + vl0) = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            __builtin_amdgcn_wave_barrier();
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-              if ((unsigned)dv[e] < (unsigned)kTile) {
-                const float zv = srow[(((dv[e] >> 2) ^ hsw16(n)) << 2) + (dv[e] & 3)];
-                cpart += bp[rr][e] * zv;
-                corr[dv[e]] = -cf * bp[rr][e];
-              }
+          for (int kb = 128; kb < K; kb += 64) {  // rows with more than 128 entries
+            const int k = kb + lane;
+            const int dv = k < K ? tidx[(int64_t)tl * K + k] - m0 : -1;
+            uint64_t mask = __ballot((unsigned)dv < (unsigned)kTile);
+            while (mask) {
+              const int src = __builtin_ctzll(mask);
+              mask &= mask - 1;
+              const int dvh = __builtin_amdgcn_readlane(dv, src);
+              const float ph = tp[(int64_t)tl * K + kb + src];
+              const int owner = dvh >> 2, comp = dvh & 3;
+              const float zc = comp == 0 ? z[0] : comp == 1 ? z[1] : comp == 2 ? z[2] : z[3];
+              cpart += ph * __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, zc), owner));
+              const float d = lane == owner ? cf * ph : 0.f;
+              if (comp == 0) G[0] -= d;
+              else if (comp == 1) G[1] -= d;
+              else if (comp == 2) G[2] -= d;
+              else G[3] -= d;
             }
-            if (K > 128) {
-              for (int k = 128 + lane; k < K; k += 64) {
-                const int d2 = tidx[(int64_t)tl * K + k] - m0;
-                if ((unsigned)d2 < (unsigned)kTile) {
-                  const float pk = tp[(int64_t)tl * K + k];
-                  const float zv = srow[(((d2 >> 2) ^ hsw16(n)) << 2) + (d2 & 3)];
-                  cpart += pk * zv;
-                  corr[d2] = -cf * pk;
-                }
-              }
-            }
-            __builtin_amdgcn_wave_barrier();
-            const f32x4_t c = *reinterpret_cast<const f32x4_t*>(corr + vl0);
-            G += c;
-            cpart = wave_sum(cpart);
           }
           if (lane == 0) part_C[(int64_t)tl * nVT + mt] = cpart;
           if (dZ != nullptr) {
