@@ -31,10 +31,9 @@ struct Plan {
   int64_t nVT;         // vocabulary tiles
   int64_t nchunks;
   int64_t nblk;        // loss partials of a full chunk (one per 64 rows)
-  int64_t G;           // chunks whose dZ^T is gathered before one dW GEMM
+  int64_t G;           // chunks whose dZ rows are gathered before one dW GEMM
   int dh_split;
-  size_t off_misc, off_p, off_rows, off_pm, off_ps, off_pc, off_lossp, off_dz, off_dzt, off_wt,
-      off_hct, off_dhs, total;
+  size_t off_misc, off_p, off_rows, off_pm, off_ps, off_pc, off_lossp, off_dz, off_dhs, total;
 };
 
 kd_status check_problem(const kd_problem* p) {
@@ -81,8 +80,11 @@ Plan make_plan(const kd_problem* p) {
   pl.nchunks = cdiv(pl.N, pl.c);
   pl.nblk = cdiv(pl.c, 64);
   // dW is accumulated in fp32 in place: each dW GEMM reads and writes all of
-  // grad_W once, so gather the dZ^T of up to ~8192 tokens per GEMM
-  pl.G = std::max<int64_t>(1, std::min<int64_t>(8192 / pl.cp, std::max<int64_t>(pl.nchunks, 1)));
+  // grad_W once, so gather the dZ rows of up to ~8192 tokens (and at most
+  // 4 GiB of dZ) per GEMM
+  pl.G = std::max<int64_t>(1, std::min<int64_t>(8192 / pl.c, std::max<int64_t>(pl.nchunks, 1)));
+  pl.G = std::max<int64_t>(
+      1, std::min<int64_t>(pl.G, ((int64_t)4 << 30) / std::max<int64_t>(pl.c * pl.Vp * pl.eb, 1)));
   const int64_t dh_tiles = cdiv(pl.c, kTile) * cdiv(pl.D, kTile);
   pl.dh_split = choose_dh_split(dh_tiles, pl.Vp * pl.eb / 128);
   size_t t = 0;
@@ -98,10 +100,7 @@ Plan make_plan(const kd_problem* p) {
   pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_pc = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
-  pl.off_dz = take((size_t)pl.cp * pl.Vp * pl.eb);
-  pl.off_dzt = take((size_t)pl.Vp * pl.G * pl.cp * pl.eb);
-  pl.off_wt = take((size_t)pl.D * pl.Vp * pl.eb);
-  pl.off_hct = take((size_t)pl.D * pl.G * pl.cp * pl.eb);
+  pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
   pl.off_dhs = pl.dh_split > 1 ? take((size_t)pl.dh_split * pl.c * pl.D * 4) : 0;
   pl.total = align256(t);
   return pl;
@@ -170,9 +169,6 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
   pa.ignore = ignore;
   pa.nvalid = nvalid;
   pa.inv_nvalid = inv_nvalid;
-  pa.W = W;
-  pa.Wt = want_dh ? ws + pl.off_wt : nullptr;
-  pa.ldw = pl.Vp;
   pa.zero_gW = (grad_W != nullptr && pl.N == 0 && !accumulate_grad_W) ? grad_W : nullptr;
   if (kd_launch_prepare(&pa, hip_stream) != 0) return KD_ERR_DEVICE;
 
@@ -207,16 +203,9 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     a.part_s = reinterpret_cast<float*>(ws + pl.off_ps);
     a.part_C = reinterpret_cast<float*>(ws + pl.off_pc);
     a.nVT = (int)pl.nVT;
-    a.dZ = want_dh ? ws + pl.off_dz : nullptr;
-    a.ldz = pl.Vp;
     const int64_t slot = ci % pl.G;
-    a.dZt = want_dw ? ws + pl.off_dzt + slot * pl.cp * pl.eb : nullptr;
-    a.ldzt = pl.G * pl.cp;
-    a.Hct = want_dw ? ws + pl.off_hct + slot * pl.cp * pl.eb : nullptr;
-    a.ldh = pl.G * pl.cp;
-    a.cp = pl.cp;
-    a.Wt = ws + pl.off_wt;
-    a.ldw = pl.Vp;
+    a.dZ = (want_dh || want_dw) ? ws + pl.off_dz + slot * pl.c * pl.Vp * pl.eb : nullptr;
+    a.ldz = pl.Vp;
     a.dh_split = pl.dh_split;
     a.dh_partial = pl.dh_split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
     a.loss_per_token = loss_per_token ? loss_per_token + row0 : nullptr;
@@ -230,11 +219,9 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
       d.dtype = p->dtype;
       d.D = pl.D;
       d.V = pl.V;
-      d.dZt = ws + pl.off_dzt;
-      d.ldzt = pl.G * pl.cp;
-      d.Hct = ws + pl.off_hct;
-      d.ldh = pl.G * pl.cp;
-      d.kcols = slot * pl.cp + cdiv(rcount, kTile) * kTile;
+      d.dZ = ws + pl.off_dz;
+      d.ldz = pl.Vp;
+      d.Hg = static_cast<const char*>(hidden) + (row0 + rcount - group_tokens) * pl.D * pl.eb;
       d.tokens = group_tokens;
       d.beta = (dw_done || accumulate_grad_W) ? 1 : 0;
       d.gW = grad_W;

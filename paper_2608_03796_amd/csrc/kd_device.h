@@ -2,10 +2,10 @@
 // resources, the XCD-aware tile order, and the 256x256 MFMA GEMM main loop
 // shared by the logits, logit-recompute, dH and dW kernels.
 //
-// GEMM convention: C[M, N] = A[M, K] * B[N, K]^T with both operands stored
-// row-major with K contiguous ("NT"). Every contraction on the hot path is
-// issued in this form; the operands that are not naturally K-contiguous (W for
-// dH, the chunk's hidden rows and dZ for dW) are supplied as transposed copies.
+// GEMM convention: C[M, N] = A[M, K] * B[N, K]^T. Each operand is read where it
+// lives, either with K contiguous along its rows (W and the hidden rows for the
+// logits, dZ for dH) or with K along its columns (W for dH, dZ and the hidden
+// rows for dW); no operand is copied or transposed in memory.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -19,6 +19,7 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
 typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2_t;
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;  // buffer resource in 4 SGPRs
 
 constexpr int kTile = 256;                       // BM = BN
 constexpr int kThreads = 512;                    // 8 waves of 64: 2 (M) x 4 (N)
@@ -96,47 +97,234 @@ __device__ __forceinline__ int acc_n(int wn, int j, int lane) { return wn * 64 +
 
 // One 256x256 output tile: acc = A[m0:m0+256, k-range] * B[n0:n0+256, k-range]^T.
 //
-// ra / rb are buffer resources based at the tile's first row, sized so rows
-// outside the operand read as zero (hardware range check). A K step is ROWB
-// bytes of every row (ROWB = 64: 32 bf16 / 16 fp32). Operands go straight from
-// memory into LDS (buffer loads with the LDS-DMA bit: no VGPR staging, no
-// ds_write) through S stages, so S-1 K steps of operand data are in flight
-// while one is consumed; one barrier per K step. The MFMA fragments of the
-// next K sub-step are read while the current sub-step's MFMAs run. The
-// caller's LDS must hold gemm_lds_bytes<ROWB, S>() bytes. Ends with a barrier,
-// so the caller may reuse the LDS.
-typedef __attribute__((address_space(3))) void lds_void_t;
+// Each operand is stored in one of two layouts:
+//  * K-contiguous (KcOp): rows are the tile's 256 M (or N) indices, K runs
+//    along the row; a K step is 128 bytes of each row. `base` points at the
+//    tile's first row and `bytes` covers only the rows that exist, so missing
+//    rows read as zeros (hardware range check).
+//  * K-major (KmOp): rows are K indices and the tile's 256 M (or N) indices run
+//    along the row; a K step is 128/sizeof(T) rows of 256 elements. `base`
+//    points at the tile's first column of K row 0 and `bytes` counts the bytes
+//    from there to the end of the last K row that exists; the resource is
+//    re-based every K step, so K rows past the end read as zeros and offsets
+//    stay 32-bit for any operand size. The MFMA fragments are read with
+//    transposing LDS reads (ds_read_b64_tr_b16: inside a 16-lane group, lane i
+//    gets element i%4 of the 8 bytes addressed by lane 4k + i/4 as its value
+//    k), so W, dZ and the hidden rows are consumed where they are.
+// Operands go straight from memory into LDS (buffer loads with the LDS-DMA
+// bit) through S stages of 32 KiB per operand; one barrier per K step; the
+// next sub-step's fragments are read while the current sub-step's MFMAs run.
+// The caller's LDS must hold kLdsMain bytes; ends with a barrier.
+//
+// The DMA loads are issued from inline assembly, so the compiler does not
+// track them: it would otherwise make every transposing LDS read wait for all
+// DMA in flight (those reads carry no alias information), which serialises the
+// prefetch of step j+2 with the reads of step j+1. Completion is ordered by
+// hand instead: s_waitcnt vmcnt before each barrier that publishes a stage.
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-template <int ROWB, int S>
-constexpr int gemm_lds_bytes() { return S * 2 * kTile * ROWB; }
-constexpr int kLdsMain = gemm_lds_bytes<kRowB, kStages>();  // 160 KiB
+constexpr int kLdsMain = kStages * 2 * kTile * kRowB;  // 128 KiB
 
-// 16-byte slot swizzle of a ROWB-byte tile row: conflict-free for the DMA
-// rows and for 8- or 16-lane groups of MFMA fragment reads.
-template <int ROWB>
-__device__ __forceinline__ int slot_swz(int row) {
-  if constexpr (ROWB == 128) return (row ^ (row >> 3)) & 7;
-  else return ((row >> 1) ^ (row >> 3)) & 3;
+struct KcOp {
+  const char* base;
+  uint32_t bytes;
+  int ld;  // row pitch in bytes
+};
+struct KmOp {
+  const char* base;
+  int64_t bytes;
+  int ld;  // row pitch in bytes
+};
+
+// 16-byte slot swizzles, chosen so the DMA rows and every 32-lane half of a
+// fragment read touch all 64 LDS banks once.
+// K-contiguous rows: 8 slots of 128 bytes.
+__device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
+// K-major bf16 rows (512 bytes, 32 slots): a transposing read covers slot
+// pairs of rows r..r+3 and r+8..r+11, which get 8 distinct even XOR values.
+__device__ __forceinline__ int swz_km16(int row) {
+  return ((row & 3) | (((row >> 3) & 1) << 2)) << 1;
 }
+// K-major fp32 rows (1 KiB, 64 slots): a 32-bit read covers 4 slots of rows
+// r, r+4, r+8, r+12, which get the XOR values 0, 4, 8, 12.
+__device__ __forceinline__ int swz_km32(int row) { return ((row >> 2) & 3) << 2; }
 
 // s_waitcnt vmcnt(n) for a compile-time n; expcnt/lgkmcnt are not waited.
 #define KD_VMCNT(n) __builtin_amdgcn_s_waitcnt((0x0f70 & ~0x000f) | ((n) & 0xf) | (((n) >> 4) << 14))
-template <typename T, int ROWB = kRowB, int S = kStages>
-__device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_bytes,
-                                          __amdgpu_buffer_rsrc_t rb, int ldb_bytes, int ks_begin,
-                                          int ks_end, char* lds, AccTile& acc) {
-  constexpr int SL = ROWB / 16;           // 16-byte slots per row
-  constexpr int SUB = SL / 4;             // MFMA sub-steps (64-byte K slices) per K step
-  constexpr int OPB = kTile * ROWB;       // one operand's stage
-  constexpr int STB = 2 * OPB;            // one stage (A and B)
-  constexpr int RPI = 1024 / ROWB;        // rows per 1 KiB DMA instruction
-  constexpr int NDMA = kTile / RPI / 8;   // DMA instructions per operand per wave
-  constexpr int NI = 2 * NDMA;            // per K step per wave (vmcnt units)
-  static_assert(SUB >= 2, "two or more sub-steps per K step");
+
+constexpr uint32_t kOobOffset = 0xfffffff0u;  // past every resource: DMA writes zeros
+
+// Raw buffer resource (stride 0, 32-bit range) in scalar registers.
+__device__ __forceinline__ i32x4_t rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  return i32x4_t{__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+                 __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32)),
+                 __builtin_amdgcn_readfirstlane((int)bytes), kRsrcWord3};
+}
+
+// One wave-wide 16-byte-per-lane LDS-DMA load: lane i's 16 bytes at voffset
+// land at LDS byte address lds_addr + 16 i. M0 is set in the same statement;
+// an LDS-DMA instruction must not directly follow an SALU write of M0 (one
+// wait state), hence the s_nop.
+__device__ __forceinline__ void dma_b128(i32x4_t r, uint32_t lds_addr, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(r)
+               : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
+}
+
+// DMA of one operand's K step: 4 instructions of 1 KiB per wave.
+template <typename T, typename Op>
+struct OpDma;
+
+template <typename T>
+struct OpDma<T, KcOp> {
+  uint32_t voff[4];
+  i32x4_t r;
+  __device__ __forceinline__ void init(const KcOp& op, int wave, int lane) {
+    r = rsrc_words(op.base, op.bytes);
+    // 8 rows of 128 bytes per instruction: lane -> row 8q + lane/8, slot lane%8
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (wave * 4 + i) * 8 + (lane >> 3);
+      voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)(((lane & 7) ^ swz_kc(row)) << 4);
+    }
+  }
+  __device__ __forceinline__ void issue(const KcOp&, char* stage, int wave, int ks,
+                                        bool live) const {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      dma_b128(r, la + i * 1024, live ? voff[i] + (uint32_t)ks * (uint32_t)kRowB : kOobOffset);
+  }
+};
+
+template <typename T>
+struct OpDma<T, KmOp> {
+  static constexpr int KS = kRowB / (int)sizeof(T);  // K rows per step
+  uint32_t voff[4];
+  __device__ __forceinline__ void init(const KmOp& op, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if constexpr (sizeof(T) == 2) {
+        // 2 K rows of 512 bytes per instruction: lane -> row 2q + lane/32, slot lane%32
+        const int row = (wave * 4 + i) * 2 + (lane >> 5);
+        voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)(((lane & 31) ^ swz_km16(row)) << 4);
+      } else {
+        // 1 K row of 1 KiB per instruction: lane -> slot lane
+        const int row = wave * 4 + i;
+        voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)((lane ^ swz_km32(row)) << 4);
+      }
+    }
+  }
+  __device__ __forceinline__ void issue(const KmOp& op, char* stage, int wave, int ks,
+                                        bool live) const {
+    const int64_t step0 = (int64_t)ks * KS * op.ld;
+    int64_t left = op.bytes - step0;
+    left = left < 0 ? 0 : (left > 0x7fffffff ? 0x7fffffff : left);
+    const i32x4_t r = rsrc_words(op.base + step0, (uint32_t)left);
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma_b128(r, la + i * 1024, live ? voff[i] : kOobOffset);
+  }
+};
+
+// Fragment reads of NB blocks of 16 rows (M or N) from `base` within the tile.
+// Sub-step s of a K step covers K elements [s*KS/2, (s+1)*KS/2) of the step;
+// lane (g = lane/16, j = lane%16) holds row base + 16b + j with K elements
+// s*KS/2 + 8g + 0..7 (bf16) or s*KS/2 + 4g + 0..3 (fp32), in both layouts.
+template <typename T, typename Op, int NB>
+struct OpFrag;
+
+template <typename T, int NB>
+struct OpFrag<T, KcOp, NB> {
+  static constexpr int kReads = NB;
+  int rd[NB], fx[NB];
+  __device__ __forceinline__ void init(int base, int lane) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int m = base + 16 * b + (lane & 15);
+      rd[b] = m * kRowB;
+      fx[b] = (lane >> 4) ^ swz_kc(m);
+    }
+  }
+  __device__ __forceinline__ void read(const char* op, int s, u32x4_t (&f)[NB]) const {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      f[b] = *reinterpret_cast<const u32x4_t*>(op + rd[b] + ((fx[b] ^ (4 * s)) << 4));
+  }
+};
+
+template <int NB>
+struct OpFrag<__bf16, KmOp, NB> {
+  static constexpr int kReads = 2 * NB;
+  static constexpr int kRow = kTile * 2;  // bytes of a K row in LDS
+  int off[NB];                            // byte offset at sub-step 0, h = 0
+  __device__ __forceinline__ void init(int base, int lane) {
+    // lane j of group g points at K row 8g + j/4 (+ 32s + 4h), columns
+    // base + 16b + 4(j%4) .. +3, so lane i receives columns base + 16b + i
+    const int g = lane >> 4, j = lane & 15;
+    const int row = 8 * g + (j >> 2);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int col = base + 16 * b + 4 * (j & 3);
+      off[b] = row * kRow + (((col >> 3) ^ swz_km16(row)) << 4) + ((col & 4) << 1);
+    }
+  }
+  __device__ __forceinline__ void read(const char* op, int s, u32x4_t (&f)[NB]) const {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      u32x2_t h0 = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                   (lds_s16x4_t*)(op + off[b] + 32 * s * kRow)));
+      u32x2_t h1 = __builtin_bit_cast(
+          u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                       (lds_s16x4_t*)(op + off[b] + (32 * s + 4) * kRow)));
+      f[b] = u32x4_t{h0[0], h0[1], h1[0], h1[1]};
+    }
+  }
+};
+
+template <int NB>
+struct OpFrag<float, KmOp, NB> {
+  static constexpr int kReads = 4 * NB;
+  static constexpr int kRow = kTile * 4;
+  int off[NB];  // byte offset of K row 4g, sub-step 0
+  __device__ __forceinline__ void init(int base, int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int row = 4 * g;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int col = base + 16 * b + j;
+      off[b] = row * kRow + (((col >> 2) ^ swz_km32(row)) << 4) + ((col & 3) << 2);
+    }
+  }
+  __device__ __forceinline__ void read(const char* op, int s, u32x4_t (&f)[NB]) const {
+    // K rows 16s + 4g + e share row 4g's swizzle (it depends on (row/4) % 4 only)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      uint32_t v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        v[e] = *reinterpret_cast<const uint32_t*>(op + off[b] + (16 * s + e) * kRow);
+      f[b] = u32x4_t{v[0], v[1], v[2], v[3]};
+    }
+  }
+};
+
+template <typename T, typename OA, typename OB>
+__device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_begin, int ks_end,
+                                          char* lds, AccTile& acc) {
+  constexpr int S = kStages;
+  constexpr int OPB = kTile * kRowB;  // one operand's stage (32 KiB)
+  constexpr int STB = 2 * OPB;        // one stage (A and B)
+  constexpr int NI = 8;               // DMA instructions per K step per wave
+  constexpr int RD = OpFrag<T, OA, 8>::kReads + OpFrag<T, OB, 4>::kReads;
+  constexpr int RQ = (RD + 15) / 16;  // LDS reads per MFMA pair
   static_assert((S - 1) * NI <= 63, "vmcnt range of the in-flight DMA steps");
-  static_assert(NDMA <= 8, "DMA offsets array");
-  // (arrays captured by the lambdas below have literal bounds: clang's host
-  // pass rejects a second instantiation when the bound is a dependent local)
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -154,58 +342,25 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
     return;
   }
 
-  // DMA instruction q (= wave*NDMA + i) fills rows [RPI*q, RPI*(q+1)) of an
-  // operand stage, 1 KiB contiguous: lane l lands at row RPI*q + l/SL,
-  // physical slot l%SL, so it fetches logical slot (l%SL) ^ swz(row).
-  uint32_t voffA[8], voffB[8];  // NDMA <= 8 used (fixed bound: see above)
-#pragma unroll
-  for (int i = 0; i < NDMA; ++i) {
-    const int row = (wave * NDMA + i) * RPI + lane / SL;
-    const uint32_t slot = (uint32_t)((lane % SL) ^ slot_swz<ROWB>(row));
-    voffA[i] = (uint32_t)row * (uint32_t)lda_bytes + slot * 16u;
-    voffB[i] = (uint32_t)row * (uint32_t)ldb_bytes + slot * 16u;
-  }
-  // fragment reads: 16x16 blocks; lane group g = lane>>4 reads logical slot
-  // 4*s + g of row (block base + lane&15) in sub-step s.
-  int rdA[8], fxA[8], rdB[4], fxB[4];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int ma = wm * 128 + 16 * i + (lane & 15);
-    rdA[i] = ma * ROWB;
-    fxA[i] = (lane >> 4) ^ slot_swz<ROWB>(ma);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int nb = wn * 64 + 16 * j + (lane & 15);
-    rdB[j] = nb * ROWB;
-    fxB[j] = (lane >> 4) ^ slot_swz<ROWB>(nb);
-  }
+  OpDma<T, OA> da;
+  OpDma<T, OB> db;
+  da.init(opa, wave, lane);
+  db.init(opb, wave, lane);
+  OpFrag<T, OA, 8> fra;
+  OpFrag<T, OB, 4> frb;
+  fra.init(wm * 128, lane);
+  frb.init(wn * 64, lane);
 
-  // DMA of K step ks into `stage`; past the last step the offset is made
-  // out of range, so the hardware fills zeros without touching memory (the
-  // schedule stays branch-free; those stages are never read).
   auto dma = [&](int ks, int stage) {
     char* a = lds + stage * STB;
-    char* b = a + OPB;
-    const uint32_t k0 = ks < ks_end ? (uint32_t)ks * ROWB : 0x80000000u;
-#pragma unroll
-    for (int i = 0; i < NDMA; ++i) {
-      const int q = wave * NDMA + i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(a + q * 1024), 16,
-                                               voffA[i] + k0, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(b + q * 1024), 16,
-                                               voffB[i] + k0, 0, 0, 0);
-    }
+    const bool live = ks < ks_end;
+    da.issue(opa, a, wave, ks, live);
+    db.issue(opb, a + OPB, wave, ks, live);
   };
   auto frag = [&](int stage, int s, u32x4_t (&fa)[8], u32x4_t (&fb)[4]) {
     const char* a = lds + stage * STB;
-    const char* b = a + OPB;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      fa[i] = *reinterpret_cast<const u32x4_t*>(a + rdA[i] + ((fxA[i] ^ (4 * s)) << 4));
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      fb[j] = *reinterpret_cast<const u32x4_t*>(b + rdB[j] + ((fxB[j] ^ (4 * s)) << 4));
+    fra.read(a, s, fa);
+    frb.read(a + OPB, s, fb);
   };
   auto mfma32 = [&](const u32x4_t (&fa)[8], const u32x4_t (&fb)[4]) {
 #pragma unroll
@@ -215,13 +370,12 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
         acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
   };
 
-  // Step j lives in stage j % S; S steps of DMA are always in flight. In
-  // step j, each of the first SUB-1 sub-steps issues the next sub-step's 12
-  // fragment reads interleaved with its 32 MFMAs. Then the wave waits for its
-  // reads and for step j+1's DMA, the barrier publishes every wave's DMA and
-  // retires stage j % S, and the last sub-step's MFMAs run interleaved with
-  // the DMA of step j+S into that stage and the fragment reads of step j+1's
-  // sub-step 0. Two waves per SIMD fill each other's waits.
+  // Step j lives in stage j % S; S steps of DMA are always in flight. Sub-step
+  // 0 reads sub-step 1's fragments interleaved with its 32 MFMAs; then the
+  // wave waits for its reads and for step j+1's DMA, the barrier publishes
+  // every wave's DMA and retires stage j % S, and sub-step 1's MFMAs run
+  // interleaved with the DMA of step j+S into that stage and the fragment
+  // reads of step j+1's sub-step 0. Two waves per SIMD fill each other's waits.
 #pragma unroll
   for (int p = 0; p < S; ++p) dma(ks_begin + p, p);
   KD_VMCNT((S - 1) * NI);
@@ -230,41 +384,29 @@ __device__ __forceinline__ void gemm_tile(__amdgpu_buffer_rsrc_t ra, int lda_byt
   frag(0, 0, fa[0], fb[0]);
   int st = 0;
   for (int j = 0; j < nsteps; ++j) {
+    frag(st, 1, fa[1], fb[1]);
+    mfma32(fa[0], fb[0]);
 #pragma unroll
-    for (int s = 0; s < SUB - 1; ++s) {
-      frag(st, s + 1, fa[(s + 1) & 1], fb[(s + 1) & 1]);
-      mfma32(fa[s & 1], fb[s & 1]);
-#pragma unroll
-      for (int q = 0; q < 12; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, RQ, 0);  // LDS read
     }
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xc07f & ~0x0f00);  // lgkmcnt(0)
     KD_VMCNT((S - 2) * NI);
     __syncthreads();
     const int nst = st + 1 == S ? 0 : st + 1;
     dma(ks_begin + j + S, st);
-    frag(nst, 0, fa[SUB & 1], fb[SUB & 1]);
-    mfma32(fa[(SUB - 1) & 1], fb[(SUB - 1) & 1]);
+    frag(nst, 0, fa[0], fb[0]);
+    mfma32(fa[1], fb[1]);
 #pragma unroll
-    for (int q = 0; q < 12; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
-      if (q < NI) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (DMA)
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);              // MFMA
+      if (q < NI) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // DMA
+      __builtin_amdgcn_sched_group_barrier(0x100, RQ, 0);             // LDS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
     st = nst;
-    if constexpr ((SUB & 1) != 0) {
-      // odd sub-step count: next step's sub-step 0 landed in buffer 1
-#pragma unroll
-      for (int i = 0; i < 8; ++i) fa[0][i] = fa[1][i];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) fb[0][i] = fb[1][i];
-    }
   }
   KD_VMCNT(0);
   __syncthreads();

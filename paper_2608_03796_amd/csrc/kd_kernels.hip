@@ -1,13 +1,14 @@
 // HIP kernels (gfx950) of the fused chunked top-K KL loss and their launchers.
 //
-// Per call:    count_valid, [W^T copy]
+// Per call:    count_valid
 // Per chunk:   teacher_prologue  -> p, M, H, g/tau                 (§3.2, Eq. 2 terms)
 //              logits_lse        -> per (token, vocab tile) max / sum-exp partials
 //              lse_merge         -> log Z per token                 (Alg. 1 normaliser)
-//              dz                -> recomputed logits, dZ = g/tau (M q - p) in LDS,
-//                                   stored as dZ[c, V] and dZ^T[V, c]; C partials
+//              dz                -> recomputed logits, dZ = g/tau (M q - p), stored
+//                                   row-major [tokens, Vp]; C partials
 //              row_loss          -> l_t = H - C/tau + M log Z       (Eq. 2)
-//              [H_c^T copy], dh (+ split reduce), dw (fp32 accumulate)
+//              dh (+ split reduce): dH_c = dZ W
+// Per group of chunks: dw        -> grad_W (+)= dZ^T H (fp32 accumulate)
 // Per call:    finalize_loss     -> mean over non-ignored tokens
 #include "kd_device.h"
 #include "kd_launch.h"
@@ -98,9 +99,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
   const int ld = D * eb;
   const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
   AccTile acc;
-  gemm_tile<T, kRowB, kStages>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
-               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowB,
-               lds, acc);
+  gemm_tile<T>(KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
+               KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld},
+               0, ld / kRowB, lds, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 2, wn = wave & 3;
@@ -186,9 +187,8 @@ __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, 
 // LDS 128 tokens at a time as [token][vocab] with a 16-byte-slot swizzle. One
 // wave per token row: G = (g/tau) M 2^(y - L2) for the dense part, the K
 // teacher entries of the row that fall in this vocabulary tile are folded in
-// (G -= (g/tau) p; C += p z), then G is stored row-major to dZ[c, Vp] and,
-// after a barrier, column-major to dZ^T[Vp, cp]. Padded token rows produce
-// zeros so dZ^T's K padding for the dW GEMM is zero.
+// (G -= (g/tau) p; C += p z), then G is stored row-major to dZ[rows, Vp]
+// (columns V..Vp hold zeros). Both dH and dW read this one copy.
 __device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
 
 template <typename T>
@@ -196,8 +196,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     const T* __restrict__ W, const T* __restrict__ Hc, int D, int V, int rows, int TM, int TN,
     float k2, const float* __restrict__ rowL2, const float* __restrict__ rowCoef,
     const float* __restrict__ rowCoefM, const int32_t* __restrict__ tidx,
-    const float* __restrict__ tp, int K, T* dZ, int64_t ldz, T* dZt, int64_t ldzt,
-    float* part_C, int nVT) {
+    const float* __restrict__ tp, int K, T* dZ, int64_t ldz, float* part_C, int nVT) {
   constexpr int kStage = 128 * 256 * 4;  // 128 token rows x 256 vocab, fp32
   constexpr int kEpi = kStage;
   __shared__ __attribute__((aligned(16))) char lds[kLdsMain > kEpi ? kLdsMain : kEpi];
@@ -208,9 +207,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   const int ld = D * eb;
   const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
   AccTile acc;
-  gemm_tile<T, kRowB, kStages>(make_rsrc(W + (int64_t)m0 * D, (uint32_t)(mrows * ld)), ld,
-               make_rsrc(Hc + (int64_t)n0 * D, (uint32_t)(nrows * ld)), ld, 0, ld / kRowB,
-               lds, acc);
+  gemm_tile<T>(KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
+               KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld},
+               0, ld / kRowB, lds, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 2, wn = wave & 3;
@@ -328,35 +327,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
             }
           }
         }
-        if (dZt != nullptr) *reinterpret_cast<f32x4_t*>(srow + myslot * 4) = G;
       }
     }
     __syncthreads();
-
-    if (dZt != nullptr) {
-      // column-major store: lane -> (vocab column, 8 consecutive tokens)
-      const int q = lane & 15;
-#pragma unroll 4
-      for (int it = 0; it < 8; ++it) {
-        const int vl = it * 32 + wave * 4 + (lane >> 4);
-        float x[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int n = 8 * q + e;
-          x[e] = st[n * 256 + ((((vl >> 2) ^ hsw16(n)) << 2) | (vl & 3))];
-        }
-        T* dst = dZt + (int64_t)(m0 + vl) * ldzt + n0 + 128 * h + 8 * q;
-        if constexpr (sizeof(T) == 2) {
-          u32x4_t w = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
-                       pack_bf16x2(x[6], x[7])};
-          *reinterpret_cast<u32x4_t*>(dst) = w;
-        } else {
-          *reinterpret_cast<f32x4_t*>(dst) = f32x4_t{x[0], x[1], x[2], x[3]};
-          *reinterpret_cast<f32x4_t*>(dst + 4) = f32x4_t{x[4], x[5], x[6], x[7]};
-        }
-      }
-      __syncthreads();
-    }
   }
 }
 
@@ -401,32 +374,14 @@ __global__ void k_finalize_loss(const float* partials, int n, const float* inv_n
   if (threadIdx.x == 0) loss[0] = red[0] * inv_nvalid[0];
 }
 
-// --------------------------------------------------------------- transpose --
-// dst[C][ldd] <- src[R][lds_]^T for r < R, zero for R <= r < Rpad (64x64 tiles).
-template <typename T>
-__global__ void k_transpose_pad(const T* __restrict__ src, int64_t R, int64_t C, int64_t lds_,
-                                T* __restrict__ dst, int64_t ldd, int64_t Rpad) {
-  __shared__ T tile[64][65];
-  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 256 threads: 64 x 4
-  for (int y = ty; y < 64; y += 4) {
-    const int64_t r = r0 + y, c = c0 + tx;
-    tile[y][tx] = (r < R && c < C) ? src[r * lds_ + c] : (T)0.0f;
-  }
-  __syncthreads();
-  for (int y = ty; y < 64; y += 4) {
-    const int64_t c = c0 + y, r = r0 + tx;
-    if (c < C && r < Rpad) dst[c * ldd + r] = tile[tx][y];
-  }
-}
-
 // -------------------------------------------------------------------- dH ----
-// dH_c[t, d] = sum_v dZ[t, v] W[v, d] as dZ[c, Vp] * (W^T[D, Vp])^T. With
+// dH_c[t, d] = sum_v dZ[t, v] W[v, d]: A = dZ (K = vocabulary contiguous),
+// B = W read K-major (rows v, columns d); rows of W past V read as zeros. With
 // split > 1 each split covers a K range and writes fp32 partials.
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, int64_t ldz,
-                                                    const T* __restrict__ Wt, int64_t ldw,
-                                                    int rows, int D, int TM, int TN, int ks_total,
+                                                    const T* __restrict__ W, int V, int rows,
+                                                    int D, int TM, int TN, int ks_total,
                                                     int split, T* gH, float* partial) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
   const int tiles = TM * TN;
@@ -435,13 +390,15 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   tile_coords(blockIdx.x - sidx * tiles, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
   const int eb = Elt<T>::bytes;
-  const int lda = (int)(ldz * eb), ldb = (int)(ldw * eb);
+  const int lda = (int)(ldz * eb), ldb = D * eb;
   const int per = (ks_total + split - 1) / split;
   const int kb = sidx * per, ke = min(ks_total, kb + per);
   AccTile acc;
-  const int mrows = min(kTile, rows - m0), nrows = min(kTile, D - n0);
-  gemm_tile<T, kRowB, kStages>(make_rsrc(dZ + (int64_t)m0 * ldz, (uint32_t)(mrows * lda)), lda,
-               make_rsrc(Wt + (int64_t)n0 * ldw, (uint32_t)(nrows * ldb)), ldb, kb, ke, lds, acc);
+  const int mrows = min(kTile, rows - m0);
+  gemm_tile<T>(KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
+               KmOp{reinterpret_cast<const char*>(W + n0),
+                    (int64_t)V * ldb - (int64_t)n0 * eb, ldb},
+               kb, ke, lds, acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 2, wn = wave & 3;
 #pragma unroll
@@ -475,24 +432,26 @@ __global__ void k_dh_reduce(const float* partial, int split, int64_t n, T* gH) {
 }
 
 // -------------------------------------------------------------------- dW ----
-// grad_W[v, d] (+)= sum_t dZ[t, v] H_c[t, d] as dZ^T[Vp, cp] * (H_c^T[D, cp])^T,
-// fp32 read-modify-write of the output tile when beta = 1.
+// grad_W[v, d] (+)= sum_t dZ[t, v] H[t, d] over the tokens of a group of
+// chunks: both operands read K-major (rows = tokens), token rows past the
+// group read as zeros; fp32 read-modify-write of the output tile when beta = 1.
 template <typename T>
-__global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZt, int64_t ldzt,
-                                                    const T* __restrict__ Hct, int64_t ldh, int V,
-                                                    int D, int TM, int TN, int ks_total, int beta,
+__global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, int64_t ldz,
+                                                    const T* __restrict__ Hg, int tokens, int V,
+                                                    int D, int TM, int TN, int beta,
                                                     float* __restrict__ gW) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
   const int eb = Elt<T>::bytes;
-  const int lda = (int)(ldzt * eb), ldb = (int)(ldh * eb);
-  const int mrows = min(kTile, V - m0), nrows = min(kTile, D - n0);
+  const int lda = (int)(ldz * eb), ldb = D * eb;
+  const int mrows = min(kTile, V - m0);
+  constexpr int KS = kRowB / (int)sizeof(T);
   AccTile acc;
-  gemm_tile<T, kRowB, kStages>(make_rsrc(dZt + (int64_t)m0 * ldzt, (uint32_t)(mrows * lda)), lda,
-               make_rsrc(Hct + (int64_t)n0 * ldh, (uint32_t)(nrows * ldb)), ldb, 0, ks_total, lds,
-               acc);
+  gemm_tile<T>(KmOp{reinterpret_cast<const char*>(dZ + m0), (int64_t)tokens * lda - (int64_t)m0 * eb, lda},
+               KmOp{reinterpret_cast<const char*>(Hg + n0), (int64_t)tokens * ldb - (int64_t)n0 * eb, ldb},
+               0, (tokens + KS - 1) / KS, lds, acc);
   // fp32 read-modify-write of the output tile through a buffer resource over
   // its rows (rows past V are out of range: loads give 0, stores are dropped);
   // each 64-value block is loaded in one batch before it is stored, so the
@@ -565,12 +524,12 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // ------------------------------------------------- event instrumentation ----
 namespace {
 enum ProfKind {
-  P_COUNT_VALID, P_TRANSPOSE_W, P_PROLOGUE, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH,
-  P_DH_REDUCE, P_TRANSPOSE_HC, P_DW, P_FINALIZE, P_FILL, P_NKINDS
+  P_COUNT_VALID, P_PROLOGUE, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE, P_DW,
+  P_FINALIZE, P_FILL, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
-    "count_valid", "transpose_W", "teacher_prologue", "logits_lse", "lse_merge", "dz",
-    "row_loss", "dh", "dh_reduce", "transpose_Hc", "dw", "finalize_loss", "fill"};
+    "count_valid", "teacher_prologue", "logits_lse", "lse_merge", "dz", "row_loss", "dh",
+    "dh_reduce", "dw", "finalize_loss", "fill"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -678,8 +637,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     ProfScope ps_(P_DZ, gemm_flops, s);
     hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
                      a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.tidx, a.p, a.K,
-                     static_cast<T*>(a.dZ), a.ldz, static_cast<T*>(a.dZt), a.ldzt, a.part_C,
-                     a.nVT);
+                     static_cast<T*>(a.dZ), a.ldz, a.part_C, a.nVT);
     }
 {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
@@ -693,9 +651,8 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
 {
     ProfScope ps_(P_DH, gemm_flops, s);
     hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.dh_split), dim3(kThreads), 0, s,
-                       static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.Wt), a.ldw,
-                       a.rows, (int)a.D, TM, TN, ks, a.dh_split, static_cast<T*>(a.gH),
-                       a.dh_partial);
+                       static_cast<const T*>(a.dZ), a.ldz, W, (int)a.V, a.rows, (int)a.D, TM, TN,
+                       ks, a.dh_split, static_cast<T*>(a.gH), a.dh_partial);
     }
     if (a.dh_split > 1) {
       const int64_t n = (int64_t)a.rows * a.D;
@@ -705,12 +662,6 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                          0, s, a.dh_partial, a.dh_split, n, static_cast<T*>(a.gH));
     }
     }
-  }
-  if (a.Hct != nullptr) {
-    // grid covers the chunk's padded column slot so H_c^T's K padding is zero
-    ProfScope ps_(P_TRANSPOSE_HC, 0.0, s);
-    hipLaunchKernelGGL(k_transpose_pad<T>, dim3(cdiv(a.cp, 64), cdiv(a.D, 64)), dim3(256), 0, s,
-                       Hc, (int64_t)a.rows, a.D, a.D, static_cast<T*>(a.Hct), a.ldh, a.cp);
   }
   return (int)hipGetLastError();
 }
@@ -723,10 +674,9 @@ extern "C" int kd_launch_chunk(const KdChunkArgs* a, void* stream) {
 template <typename T>
 static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
   const int TM = cdiv(a.V, kTile), TN = cdiv(a.D, kTile);
-  const int ks = (int)(a.kcols * (int64_t)sizeof(T) / kRowB);
   ProfScope ps_(P_DW, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
-  hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s, static_cast<const T*>(a.dZt),
-                     a.ldzt, static_cast<const T*>(a.Hct), a.ldh, (int)a.V, (int)a.D, TM, TN, ks,
+  hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s, static_cast<const T*>(a.dZ),
+                     a.ldz, static_cast<const T*>(a.Hg), (int)a.tokens, (int)a.V, (int)a.D, TM, TN,
                      a.beta, a.gW);
   return (int)hipGetLastError();
 }
@@ -743,18 +693,6 @@ extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
     hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(256), 0, s, a->ignore, a->N, a->nvalid,
                      a->inv_nvalid);
     }
-  if (a->Wt != nullptr) {
-    ProfScope ps_(P_TRANSPOSE_W, 0.0, s);
-    const dim3 grid(cdiv(a->ldw, 64), cdiv(a->D, 64));  // includes the zero padding
-    if (a->dtype == 1)
-      hipLaunchKernelGGL(k_transpose_pad<__bf16>, grid, dim3(256), 0, s,
-                         static_cast<const __bf16*>(a->W), a->V, a->D, a->D,
-                         static_cast<__bf16*>(a->Wt), a->ldw, a->ldw);
-    else
-      hipLaunchKernelGGL(k_transpose_pad<float>, grid, dim3(256), 0, s,
-                         static_cast<const float*>(a->W), a->V, a->D, a->D,
-                         static_cast<float*>(a->Wt), a->ldw, a->ldw);
-  }
   if (a->zero_gW != nullptr) {
     const int64_t n = a->V * a->D;
 {

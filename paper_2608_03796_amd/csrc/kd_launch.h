@@ -11,9 +11,6 @@ struct KdPrepareArgs {
   const uint8_t* ignore;    // [N] or null
   int* nvalid;              // device int
   float* inv_nvalid;        // device float: 1/N_valid or 0
-  const void* W;            // [V, D]
-  void* Wt;                 // [D, ldw] or null (no dH requested)
-  int64_t ldw;              // padded vocabulary (multiple of 256)
   float* zero_gW;           // grad_W to clear, or null
 };
 
@@ -35,15 +32,8 @@ struct KdChunkArgs {
   float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
   float *part_m, *part_s, *part_C;                   // [rows, nVT]
   int nVT;
-  void* dZ;                 // [cp, ldz] or null (no dH)
-  int64_t ldz;              // = padded vocabulary
-  void* dZt;                // this chunk's column slot of dZ^T [ldz, ldzt], or null
-  int64_t ldzt;             // = chunks per dW group * padded chunk
-  void* Hct;                // this chunk's column slot of H^T [D, ldh], or null
-  int64_t ldh;              // = ldzt
-  int64_t cp;               // padded chunk (width of a column slot)
-  const void* Wt;           // [D, ldw] (dH)
-  int64_t ldw;
+  void* dZ;                 // this chunk's rows of the group's dZ [rows, ldz]
+  int64_t ldz;              // = padded vocabulary (columns V..ldz are written as 0)
   int dh_split;
   float* dh_partial;        // [dh_split, rows, D] when dh_split > 1
   // outputs
@@ -52,16 +42,14 @@ struct KdChunkArgs {
   void* gH;                 // grad_hidden + row0 * D, or null
 };
 
-// dW GEMM over the chunks of one group: grad_W (+)= dZ^T[:, :kcols] H^T[:, :kcols]^T
+// dW GEMM over the chunks of one group: grad_W (+)= dZ[:tokens]^T H[:tokens]
 struct KdDwArgs {
   int dtype;
   int64_t D, V;
-  const void* dZt;          // [Vp, ldzt]
-  int64_t ldzt;
-  const void* Hct;          // [D, ldh]
-  int64_t ldh;
-  int64_t kcols;            // columns of the group holding data (multiple of 256)
-  int64_t tokens;           // tokens in the group (for the FLOP count)
+  const void* dZ;           // the group's dZ rows [tokens, ldz]
+  int64_t ldz;
+  const void* Hg;           // the group's hidden rows [tokens, D]
+  int64_t tokens;           // tokens in the group
   int beta;                 // 0 overwrite, 1 accumulate
   float* gW;
 };
