@@ -177,7 +177,16 @@ __device__ __forceinline__ uint32_t lds_addr(const char* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
 }
 
-// DMA of one operand's K step: 4 instructions of 1 KiB per wave.
+// DMA of one operand's K step: 4 instructions of 1 KiB per wave. prep()
+// computes the step's resource, LDS address and offsets; one(i) issues
+// instruction i.
+struct DmaStep {
+  i32x4_t r;
+  uint32_t la;
+  uint32_t off[4];
+  __device__ __forceinline__ void one(int i) const { dma_b128(r, la + i * 1024, off[i]); }
+};
+
 template <typename T, typename Op>
 struct OpDma;
 
@@ -194,12 +203,15 @@ struct OpDma<T, KcOp> {
       voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)(((lane & 7) ^ swz_kc(row)) << 4);
     }
   }
-  __device__ __forceinline__ void issue(const KcOp&, char* stage, int wave, int ks,
-                                        bool live) const {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
+  __device__ __forceinline__ DmaStep prep(const KcOp&, char* stage, int wave, int ks,
+                                          bool live) const {
+    DmaStep d;
+    d.r = r;
+    d.la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      dma_b128(r, la + i * 1024, live ? voff[i] + (uint32_t)ks * (uint32_t)kRowB : kOobOffset);
+      d.off[i] = live ? voff[i] + (uint32_t)ks * (uint32_t)kRowB : kOobOffset;
+    return d;
   }
 };
 
@@ -221,15 +233,17 @@ struct OpDma<T, KmOp> {
       }
     }
   }
-  __device__ __forceinline__ void issue(const KmOp& op, char* stage, int wave, int ks,
-                                        bool live) const {
+  __device__ __forceinline__ DmaStep prep(const KmOp& op, char* stage, int wave, int ks,
+                                          bool live) const {
     const int64_t step0 = (int64_t)ks * KS * op.ld;
     int64_t left = op.bytes - step0;
     left = left < 0 ? 0 : (left > 0x7fffffff ? 0x7fffffff : left);
-    const i32x4_t r = rsrc_words(op.base + step0, (uint32_t)left);
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
+    DmaStep d;
+    d.r = rsrc_words(op.base + step0, (uint32_t)left);
+    d.la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma_b128(r, la + i * 1024, live ? voff[i] : kOobOffset);
+    for (int i = 0; i < 4; ++i) d.off[i] = live ? voff[i] : kOobOffset;
+    return d;
   }
 };
 
@@ -252,10 +266,8 @@ struct OpFrag<T, KcOp, NB> {
       fx[b] = (lane >> 4) ^ swz_kc(m);
     }
   }
-  __device__ __forceinline__ void read(const char* op, int s, u32x4_t (&f)[NB]) const {
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-      f[b] = *reinterpret_cast<const u32x4_t*>(op + rd[b] + ((fx[b] ^ (4 * s)) << 4));
+  __device__ __forceinline__ u32x4_t one(const char* op, int s, int b) const {
+    return *reinterpret_cast<const u32x4_t*>(op + rd[b] + ((fx[b] ^ (4 * s)) << 4));
   }
 };
 
@@ -275,16 +287,12 @@ struct OpFrag<__bf16, KmOp, NB> {
       off[b] = row * kRow + (((col >> 3) ^ swz_km16(row)) << 4) + ((col & 4) << 1);
     }
   }
-  __device__ __forceinline__ void read(const char* op, int s, u32x4_t (&f)[NB]) const {
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      u32x2_t h0 = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                                   (lds_s16x4_t*)(op + off[b] + 32 * s * kRow)));
-      u32x2_t h1 = __builtin_bit_cast(
-          u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                       (lds_s16x4_t*)(op + off[b] + (32 * s + 4) * kRow)));
-      f[b] = u32x4_t{h0[0], h0[1], h1[0], h1[1]};
-    }
+  __device__ __forceinline__ u32x4_t one(const char* op, int s, int b) const {
+    u32x2_t h0 = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                 (lds_s16x4_t*)(op + off[b] + 32 * s * kRow)));
+    u32x2_t h1 = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                 (lds_s16x4_t*)(op + off[b] + (32 * s + 4) * kRow)));
+    return u32x4_t{h0[0], h0[1], h1[0], h1[1]};
   }
 };
 
@@ -302,16 +310,13 @@ struct OpFrag<float, KmOp, NB> {
       off[b] = row * kRow + (((col >> 2) ^ swz_km32(row)) << 4) + ((col & 3) << 2);
     }
   }
-  __device__ __forceinline__ void read(const char* op, int s, u32x4_t (&f)[NB]) const {
+  __device__ __forceinline__ u32x4_t one(const char* op, int s, int b) const {
     // K rows 16s + 4g + e share row 4g's swizzle (it depends on (row/4) % 4 only)
+    uint32_t v[4];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      uint32_t v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        v[e] = *reinterpret_cast<const uint32_t*>(op + off[b] + (16 * s + e) * kRow);
-      f[b] = u32x4_t{v[0], v[1], v[2], v[3]};
-    }
+    for (int e = 0; e < 4; ++e)
+      v[e] = *reinterpret_cast<const uint32_t*>(op + off[b] + (16 * s + e) * kRow);
+    return u32x4_t{v[0], v[1], v[2], v[3]};
   }
 };
 
@@ -323,7 +328,7 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
   constexpr int STB = 2 * OPB;        // one stage (A and B)
   constexpr int NI = 8;               // DMA instructions per K step per wave
   constexpr int RD = OpFrag<T, OA, 8>::kReads + OpFrag<T, OB, 4>::kReads;
-  constexpr int RQ = (RD + 15) / 16;  // LDS reads per MFMA pair
+  constexpr int RQ = (RD + 15) / 16;  // LDS reads per MFMA pair in sub-step 0
   static_assert((S - 1) * NI <= 63, "vmcnt range of the in-flight DMA steps");
 
   const int tid = threadIdx.x;
@@ -351,33 +356,37 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
   fra.init(wm * 128, lane);
   frb.init(wn * 64, lane);
 
-  auto dma = [&](int ks, int stage) {
-    char* a = lds + stage * STB;
-    const bool live = ks < ks_end;
-    da.issue(opa, a, wave, ks, live);
-    db.issue(opb, a + OPB, wave, ks, live);
-  };
   auto frag = [&](int stage, int s, u32x4_t (&fa)[8], u32x4_t (&fb)[4]) {
     const char* a = lds + stage * STB;
-    fra.read(a, s, fa);
-    frb.read(a + OPB, s, fb);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) fa[b] = fra.one(a, s, b);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) fb[b] = frb.one(a + OPB, s, b);
   };
-  auto mfma32 = [&](const u32x4_t (&fa)[8], const u32x4_t (&fb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
+  auto mfma2 = [&](int q, const u32x4_t (&fa)[8], const u32x4_t (&fb)[4]) {
+    const int i = q >> 1, j = 2 * (q & 1);
+    acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
+    acc.v[i][j + 1] = mfma_slot(fa[i], fb[j + 1], acc.v[i][j + 1], (T*)nullptr);
   };
 
   // Step j lives in stage j % S; S steps of DMA are always in flight. Sub-step
-  // 0 reads sub-step 1's fragments interleaved with its 32 MFMAs; then the
-  // wave waits for its reads and for step j+1's DMA, the barrier publishes
-  // every wave's DMA and retires stage j % S, and sub-step 1's MFMAs run
-  // interleaved with the DMA of step j+S into that stage and the fragment
-  // reads of step j+1's sub-step 0. Two waves per SIMD fill each other's waits.
+  // 0's 32 MFMAs run interleaved with the reads of sub-step 1's fragments;
+  // then the wave waits for its reads and for step j+1's DMA, the barrier
+  // publishes every wave's DMA and retires stage j % S, and sub-step 1's MFMAs
+  // run in 16 pairs, each pair issued with one DMA instruction of step j+S
+  // (into the retired stage) and one fragment of step j+1's sub-step 0. Two
+  // waves per SIMD fill each other's waits.
 #pragma unroll
-  for (int p = 0; p < S; ++p) dma(ks_begin + p, p);
+  for (int p = 0; p < S; ++p) {
+    char* a = lds + p * STB;
+    const bool live = ks_begin + p < ks_end;
+    const DmaStep sa = da.prep(opa, a, wave, ks_begin + p, live);
+    const DmaStep sb = db.prep(opb, a + OPB, wave, ks_begin + p, live);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sa.one(i);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sb.one(i);
+  }
   KD_VMCNT((S - 1) * NI);
   __syncthreads();
   u32x4_t fa[2][8], fb[2][4];
@@ -385,7 +394,8 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
   int st = 0;
   for (int j = 0; j < nsteps; ++j) {
     frag(st, 1, fa[1], fb[1]);
-    mfma32(fa[0], fb[0]);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) mfma2(q, fa[0], fb[0]);
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
@@ -396,16 +406,22 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
     KD_VMCNT((S - 2) * NI);
     __syncthreads();
     const int nst = st + 1 == S ? 0 : st + 1;
-    dma(ks_begin + j + S, st);
-    frag(nst, 0, fa[0], fb[0]);
-    mfma32(fa[1], fb[1]);
+    {
+      char* a = lds + st * STB;
+      const char* n = lds + nst * STB;
+      const int ks = ks_begin + j + S;
+      const DmaStep sa = da.prep(opa, a, wave, ks, ks < ks_end);
+      const DmaStep sb = db.prep(opb, a + OPB, wave, ks, ks < ks_end);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);              // MFMA
-      if (q < NI) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // DMA
-      __builtin_amdgcn_sched_group_barrier(0x100, RQ, 0);             // LDS read
+      for (int q = 0; q < 16; ++q) {
+        if (q < 4) sa.one(q);
+        else if (q < 8) sb.one(q - 4);
+        mfma2(q, fa[1], fb[1]);
+        if (q < 8) fa[0][q] = fra.one(n, 0, q);
+        else if (q < 12) fb[0][q - 8] = frb.one(n + OPB, 0, q - 8);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    __builtin_amdgcn_sched_barrier(0);
     st = nst;
   }
   KD_VMCNT(0);
