@@ -33,7 +33,8 @@ struct Plan {
   int64_t nblk;        // loss partials of a full chunk (one per 64 rows)
   int64_t G;           // chunks whose dZ rows are gathered before one dW GEMM
   int dh_split;
-  size_t off_misc, off_p, off_rows, off_pm, off_ps, off_pc, off_lossp, off_dz, off_dhs, total;
+  size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
+      off_lossp, off_dz, off_dhs, total;
 };
 
 kd_status check_problem(const kd_problem* p) {
@@ -80,9 +81,9 @@ Plan make_plan(const kd_problem* p) {
   pl.nchunks = cdiv(pl.N, pl.c);
   pl.nblk = cdiv(pl.c, 64);
   // dW is accumulated in fp32 in place: each dW GEMM reads and writes all of
-  // grad_W once, so gather the dZ rows of up to ~8192 tokens (and at most
+  // grad_W once, so gather the dZ rows of up to ~16384 tokens (and at most
   // 4 GiB of dZ) per GEMM
-  pl.G = std::max<int64_t>(1, std::min<int64_t>(8192 / pl.c, std::max<int64_t>(pl.nchunks, 1)));
+  pl.G = std::max<int64_t>(1, std::min<int64_t>(16384 / pl.c, std::max<int64_t>(pl.nchunks, 1)));
   pl.G = std::max<int64_t>(
       1, std::min<int64_t>(pl.G, ((int64_t)4 << 30) / std::max<int64_t>(pl.c * pl.Vp * pl.eb, 1)));
   const int64_t dh_tiles = cdiv(pl.c, kTile) * cdiv(pl.D, kTile);
@@ -98,7 +99,10 @@ Plan make_plan(const kd_problem* p) {
   pl.off_rows = take((size_t)6 * pl.cp * 4);
   pl.off_pm = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
-  pl.off_pc = take((size_t)pl.cp * pl.nVT * 4);
+  pl.off_hits = take((size_t)pl.cp * pl.K * 4);
+  pl.off_hitp = take((size_t)pl.cp * pl.K * 4);
+  pl.off_hoff = take((size_t)(pl.cp / kTile) * (pl.nVT + 1) * 4);
+  pl.off_zhit = take((size_t)pl.cp * pl.K * 4);
   pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
   pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
   pl.off_dhs = pl.dh_split > 1 ? take((size_t)pl.dh_split * pl.c * pl.D * 4) : 0;
@@ -201,7 +205,10 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     a.rowL2 = rows + 4 * pl.cp;
     a.part_m = reinterpret_cast<float*>(ws + pl.off_pm);
     a.part_s = reinterpret_cast<float*>(ws + pl.off_ps);
-    a.part_C = reinterpret_cast<float*>(ws + pl.off_pc);
+    a.hits = reinterpret_cast<uint32_t*>(ws + pl.off_hits);
+    a.hitp = reinterpret_cast<float*>(ws + pl.off_hitp);
+    a.hoff = reinterpret_cast<int*>(ws + pl.off_hoff);
+    a.zhit = reinterpret_cast<float*>(ws + pl.off_zhit);
     a.nVT = (int)pl.nVT;
     const int64_t slot = ci % pl.G;
     a.dZ = (want_dh || want_dw) ? ws + pl.off_dz + slot * pl.c * pl.Vp * pl.eb : nullptr;

@@ -36,6 +36,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
                                            kRsrcWord3);
 }
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar) value:
+// loops and branches on it stay scalar instead of running under an exec mask.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs (pid % 8). Give each
 // XCD a contiguous range of the linear tile order, so the ~32 tiles an XCD runs
 // at once are neighbours and share operand rows in that XCD's L2; inside the
@@ -169,6 +175,13 @@ __device__ __forceinline__ i32x4_t rsrc_words(const void* base, uint32_t bytes) 
 // wait state), hence the s_nop.
 __device__ __forceinline__ void dma_b128(i32x4_t r, uint32_t lds_addr, uint32_t voff) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(r)
+               : "memory");
+}
+// 4-byte-per-lane LDS-DMA load: lane i's dword at voffset lands at lds_addr + 4 i.
+__device__ __forceinline__ void dma_b32(i32x4_t r, uint32_t lds_addr, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
                :
                : "s"(lds_addr), "v"(voff), "s"(r)
                : "memory");
@@ -333,7 +346,7 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
 
 #pragma unroll
@@ -440,17 +453,25 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
+// inclusive prefix sum over the 64 lanes of a wave
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// round-to-nearest-even fp32 -> bf16 bits
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  if ((u & 0x7f800000u) == 0x7f800000u) return (u >> 16) | ((u & 0xffffu) ? 0x40u : 0u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
-}
+// two fp32 -> packed bf16 (v_cvt_pk_bf16_f32, round to nearest even)
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return bf16_bits(lo) | (bf16_bits(hi) << 16);
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
+
 
 }  // namespace kd

@@ -4,8 +4,9 @@
 // Per chunk:   teacher_prologue  -> p, M, H, g/tau                 (§3.2, Eq. 2 terms)
 //              logits_lse        -> per (token, vocab tile) max / sum-exp partials
 //              lse_merge         -> log Z per token                 (Alg. 1 normaliser)
+//              bucket            -> teacher entries grouped by vocabulary tile
 //              dz                -> recomputed logits, dZ = g/tau (M q - p), stored
-//                                   row-major [tokens, Vp]; C partials
+//                                   row-major [tokens, Vp]; z at the teacher entries
 //              row_loss          -> l_t = H - C/tau + M log Z       (Eq. 2)
 //              dh (+ split reduce): dH_c = dZ W
 // Per group of chunks: dw        -> grad_W (+)= dZ^T H (fp32 accumulate)
@@ -48,7 +49,7 @@ __global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, i
                                    float* p_out, float* rowM, float* rowH, float* rowCoef,
                                    float* rowCoefM) {
   const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
   const int64_t t = row0 + r;
   const float* u = tlogit + t * (int64_t)K;
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
                KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld},
                0, ld / kRowB, lds, acc);
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
   const bool full = m0 + kTile <= V;
   float* xch = reinterpret_cast<float*>(lds);  // [wn][j][16 lanes][max, sum]
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
 __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, int nVT,
                             float* rowL2) {
   const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
   const float* pm = part_m + (int64_t)r * nVT;
   const float* ps = part_s + (int64_t)r * nVT;
@@ -182,41 +183,155 @@ __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, 
   if (lane == 0) rowL2[r] = mx + log2f(s);
 }
 
+// ------------------------------------------------ teacher entry buckets ----
+// The K cached entries of each token are folded into the dZ tile that holds
+// their vocabulary column (§3.2). One workgroup per 256-token tile groups the
+// tile's entries by vocabulary tile with a counting sort in LDS: segment nt of
+// `hits` (capacity 256 K) lists, for vocabulary tile b, the entries
+// [hoff[nt][b], hoff[nt][b+1]) as (token in tile | column in tile << 8 | k << 16)
+// with their teacher probability in `hitp`. An index outside [0, V) gets no
+// slot and a zero z (it contributes nothing to C or dZ).
+constexpr int kBucketThreads = 1024;
+constexpr int kMaxVT = 4096;  // vocabulary tiles (V <= 2^20)
+
+__global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __restrict__ tidx,
+                                                           const float* __restrict__ p, int rows,
+                                                           int K, int V, int nVT, uint32_t* hits,
+                                                           float* hitp, int* hoff, float* zhit) {
+  __shared__ int cnt[kMaxVT];
+  __shared__ int cur[kMaxVT];
+  __shared__ int wsum[kBucketThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int t0 = blockIdx.x * kTile;
+  const int total = min(kTile, rows - t0) * K;
+  const int64_t seg = (int64_t)blockIdx.x * kTile * K;
+  for (int b = tid; b < nVT; b += kBucketThreads) cnt[b] = 0;
+  __syncthreads();
+  for (int e = tid; e < total; e += kBucketThreads) {
+    const int tl = e / K, k = e - tl * K;
+    const int64_t g = (int64_t)(t0 + tl) * K + k;
+    const int v = tidx[g];
+    if ((unsigned)v < (unsigned)V)
+      atomicAdd(&cnt[v >> 8], 1);
+    else
+      zhit[g] = 0.f;
+  }
+  __syncthreads();
+  // exclusive scan: thread tid owns bins [tid R, tid R + R)
+  const int R = (nVT + kBucketThreads - 1) / kBucketThreads;
+  int run = 0;
+  for (int q = 0; q < R; ++q) {
+    const int b = tid * R + q;
+    if (b < nVT) run += cnt[b];
+  }
+  const int incl = wave_incl_scan(run);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    const int x = lane < kBucketThreads / 64 ? wsum[lane] : 0;
+    const int y = wave_incl_scan(x);
+    if (lane < kBucketThreads / 64) wsum[lane] = y - x;
+  }
+  __syncthreads();
+  int off = wsum[wave] + incl - run;
+  int* ho = hoff + (int64_t)blockIdx.x * (nVT + 1);
+  for (int q = 0; q < R; ++q) {
+    const int b = tid * R + q;
+    if (b < nVT) {
+      cur[b] = off;
+      ho[b] = off;
+      off += cnt[b];
+    }
+  }
+  if (tid == kBucketThreads - 1) ho[nVT] = off;
+  __syncthreads();
+  for (int e = tid; e < total; e += kBucketThreads) {
+    const int tl = e / K, k = e - tl * K;
+    const int64_t g = (int64_t)(t0 + tl) * K + k;
+    const int v = tidx[g];
+    if ((unsigned)v < (unsigned)V) {
+      const int pos = atomicAdd(&cur[v >> 8], 1);
+      hits[seg + pos] = (uint32_t)tl | ((uint32_t)(v & 255) << 8) | ((uint32_t)k << 16);
+      hitp[seg + pos] = p[g];
+    }
+  }
+}
+
 // --------------------------------------- logit recompute + dZ epilogue -----
-// Same tile as k_logits_lse (bitwise identical z). The fp32 tile is staged in
-// LDS 128 tokens at a time as [token][vocab] with a 16-byte-slot swizzle. One
-// wave per token row: G = (g/tau) M 2^(y - L2) for the dense part, the K
-// teacher entries of the row that fall in this vocabulary tile are folded in
-// (G -= (g/tau) p; C += p z), then G is stored row-major to dZ[rows, Vp]
-// (columns V..Vp hold zeros). Both dH and dW read this one copy.
+// Same tile as k_logits_lse (bitwise identical z). Before the main loop the
+// tile's per-token scalars (g/tau M, g/tau, log2 Z) and its bucket of teacher
+// entries are copied into spare LDS by DMA, so the epilogue issues no global
+// loads (a load waited for after a store would also wait for that store).
+// The fp32 tile is staged 128 tokens at a time as [token][vocab] with a
+// 16-byte-slot swizzle; each teacher entry of the half is patched in place to
+// its final value (g/tau)(M q - p), its z is recorded for C, and a bitmap marks
+// it; then one wave per token row forms G = (g/tau) M 2^(y - L2) elsewhere and
+// stores the row of dZ[rows, Vp] (columns V..Vp as zeros).
 __device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
+
+constexpr int kDzRows = kLdsMain;             // 3 x 256 floats: g/tau M, g/tau, log2 Z
+constexpr int kDzHits = kDzRows + 3 * 1024;   // kDzHitCap entries, then their p
+constexpr int kDzHitCap = 512;
+constexpr int kDzBits = kDzHits + 8 * kDzHitCap;  // 128 x 256-bit hit map of one half
+constexpr int kDzLds = kDzBits + 4 * 1024;
 
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_dz(
     const T* __restrict__ W, const T* __restrict__ Hc, int D, int V, int rows, int TM, int TN,
     float k2, const float* __restrict__ rowL2, const float* __restrict__ rowCoef,
-    const float* __restrict__ rowCoefM, const int32_t* __restrict__ tidx,
-    const float* __restrict__ tp, int K, T* dZ, int64_t ldz, float* part_C, int nVT) {
-  constexpr int kStage = 128 * 256 * 4;  // 128 token rows x 256 vocab, fp32
-  constexpr int kEpi = kStage;
-  __shared__ __attribute__((aligned(16))) char lds[kLdsMain > kEpi ? kLdsMain : kEpi];
+    const float* __restrict__ rowCoefM, const uint32_t* __restrict__ hits,
+    const float* __restrict__ hitp, const int* __restrict__ hoff, int K, int nVT, T* dZ,
+    int64_t ldz, float* zhit) {
+  __shared__ __attribute__((aligned(16))) char lds[kDzLds];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
   const int eb = Elt<T>::bytes;
   const int ld = D * eb;
   const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wm = wave >> 2, wn = wave & 3;
+
+  // this tile's bucket of teacher entries
+  const int64_t seg = (int64_t)nt * kTile * K;
+  const int* ho = hoff + (int64_t)nt * (nVT + 1) + mt;
+  const int hb = ho[0], cnt = ho[1] - hb;
+  if (wave < 3) {
+    const float* src = wave == 0 ? rowCoefM : wave == 1 ? rowCoef : rowL2;
+    dma_b128(rsrc_words(src + n0, (uint32_t)nrows * 4u),
+             __builtin_amdgcn_readfirstlane(lds_addr(lds + kDzRows + wave * 1024)), lane * 16);
+  } else if (wave < 7) {
+    // waves 3, 4: entries [0, 256), [256, 512); waves 5, 6: their p
+    const int part = (wave - 3) & 1;
+    const char* src = wave < 5 ? reinterpret_cast<const char*>(hits + seg)
+                               : reinterpret_cast<const char*>(hitp + seg);
+    const i32x4_t r = rsrc_words(src, (uint32_t)(hb + cnt) * 4u);
+    const uint32_t la = __builtin_amdgcn_readfirstlane(
+        lds_addr(lds + kDzHits + (wave < 5 ? 0 : 4 * kDzHitCap) + part * 1024));
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      dma_b32(r, la + q * 256, (uint32_t)(hb + part * 256 + q * 64 + lane) * 4u);
+  }
+
   AccTile acc;
   gemm_tile<T>(KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
                KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld},
                0, ld / kRowB, lds, acc);
+  KD_VMCNT(0);  // the prefetch above (published by the first barrier below)
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
   float* st = reinterpret_cast<float*>(lds);
+  const float* rs_cm = reinterpret_cast<const float*>(lds + kDzRows);
+  const float* rs_cf = rs_cm + 256;
+  const float* rs_l2 = rs_cm + 512;
+  const uint32_t* hl = reinterpret_cast<const uint32_t*>(lds + kDzHits);
+  const float* hp = reinterpret_cast<const float*>(lds + kDzHits + 4 * kDzHitCap);
+  uint32_t* hbits = reinterpret_cast<uint32_t*>(lds + kDzBits);
   const int vl0 = 4 * lane;  // this lane's 4 vocabulary columns in the row pass
   const bool vfull = m0 + kTile <= V;
 
+  // unrolled: a loop header here would make the compiler wait for the first
+  // half's dZ stores before staging the second half
+#pragma unroll
   for (int h = 0; h < 2; ++h) {
     if ((wn >> 1) == h) {
 #pragma unroll
@@ -229,103 +344,50 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
           *reinterpret_cast<f32x4_t*>(st + n * 256 + slot * 4) = acc.v[i][j];
         }
     }
+    hbits[tid] = 0u;
+    hbits[tid + kThreads] = 0u;
     __syncthreads();
 
-    // per-row scalars of this wave's 16 rows, lane rr holding row rr
-    const int tl_lane = n0 + 128 * h + wave * 16 + (lane & 15);
-    float my_cm = 0.f, my_cf = 0.f, my_l2 = 0.f;
-    if (tl_lane < rows) {
-      my_cm = rowCoefM[tl_lane];
-      my_cf = rowCoef[tl_lane];
-      my_l2 = rowL2[tl_lane];
-    }
-    for (int b8 = 0; b8 < 2; ++b8) {
-      // the first 128 teacher entries of 8 rows, loaded in one batch
-      int bi[8][2];
-      float bp[8][2];
+    // Teacher entries of this half: dZ = (g/tau) M q - (g/tau) p in place,
+    // z kept for C = sum_k p z (Eq. 2). The first kDzHitCap entries come from
+    // the LDS copy; a skewed teacher with more entries in one tile reads the
+    // rest from memory.
+    auto fold = [&](uint32_t e, float pk) {
+      const int tl = (int)(e & 255u);
+      if ((tl >> 7) != h) return;
+      const int n = tl & 127, v = (int)((e >> 8) & 255u), k = (int)(e >> 16);
+      float* cell = st + n * 256 + ((((v >> 2) ^ hsw16(n)) << 2) | (v & 3));
+      const float z = *cell;
+      zhit[(int64_t)(n0 + tl) * K + k] = z;
+      *cell = rs_cm[tl] * fast_exp2(z * k2 - rs_l2[tl]) - rs_cf[tl] * pk;
+      atomicOr(&hbits[n * 8 + (v >> 5)], 1u << (v & 31));
+    };
+    for (int q = tid; q < min(cnt, kDzHitCap); q += kThreads) fold(hl[q], hp[q]);
+    for (int q = kDzHitCap + tid; q < cnt; q += kThreads) fold(hits[seg + hb + q], hitp[seg + hb + q]);
+    __syncthreads();
+
+    if (dZ != nullptr) {
+#pragma unroll 4
+      for (int rr = 0; rr < 16; ++rr) {
+        const int n = wave * 16 + rr;
+        const int tl = 128 * h + n;  // token row within the tile
+        if (n0 + tl >= rows) break;
+        const f32x4_t z = *reinterpret_cast<const f32x4_t*>(st + n * 256 + ((lane ^ hsw16(n)) << 2));
+        const uint32_t mark = (hbits[n * 8 + (lane >> 3)] >> ((lane & 7) * 4)) & 15u;
+        const float cm = rs_cm[tl], L2 = rs_l2[tl];
+        f32x4_t G;
 #pragma unroll
-      for (int rr = 0; rr < 8; ++rr) {
-        const int tl = n0 + 128 * h + wave * 16 + b8 * 8 + rr;
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int k = 64 * e + lane;
-          const bool ok = tl < rows && k < K;
-          bi[rr][e] = ok ? tidx[(int64_t)tl * K + k] : -1;
-          bp[rr][e] = ok ? tp[(int64_t)tl * K + k] : 0.f;
+        for (int e = 0; e < 4; ++e) {
+          const bool ok = vfull || (m0 + vl0 + e < V);
+          const float dense = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
+          G[e] = (mark >> e) & 1u ? z[e] : dense;
         }
-      }
-#pragma unroll
-      for (int rr = 0; rr < 8; ++rr) {
-        const int n = wave * 16 + b8 * 8 + rr;
-        const int tl = n0 + 128 * h + n;  // token row within the chunk
-        float* srow = st + n * 256;
-        const int myslot = lane ^ hsw16(n);
-        f32x4_t G = {0.f, 0.f, 0.f, 0.f};
-        if (tl < rows) {
-          const f32x4_t z = *reinterpret_cast<const f32x4_t*>(srow + myslot * 4);
-          const int src = b8 * 8 + rr;
-          const float cm = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cm), src));
-          const float cf = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_cf), src));
-          const float L2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, my_l2), src));
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool ok = vfull || (m0 + vl0 + e < V);
-            G[e] = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
-          }
-          // Teacher entries of this row inside [m0, m0 + 256) (distinct indices,
-          // each ~0.2 per row per tile): a ballot over the lanes holding entries,
-          // then a scalar loop over the hits in lane order. Column dv lives in
-          // lane dv/4, component dv%4: that lane subtracts (g/tau) p, and the
-          // row's C partial sum_hits p * z is formed from z read across lanes.
-          float cpart = 0.f;
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const int dv = bi[rr][e] - m0;
-            uint64_t mask = __ballot((unsigned)dv < (unsigned)kTile);
-            while (mask) {
-              const int src = __builtin_ctzll(mask);
-              mask &= mask - 1;
-              const int dvh = __builtin_amdgcn_readlane(dv, src);
-              const float ph = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bp[rr][e]), src));
-              const int owner = dvh >> 2, comp = dvh & 3;
-              const float zc = comp == 0 ? z[0] : comp == 1 ? z[1] : comp == 2 ? z[2] : z[3];
-              cpart += ph * __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, zc), owner));
-              const float d = lane == owner ? cf * ph : 0.f;
-              if (comp == 0) G[0] -= d;
-              else if (comp == 1) G[1] -= d;
-              else if (comp == 2) G[2] -= d;
-              else G[3] -= d;
-            }
-          }
-          for (int kb = 128; kb < K; kb += 64) {  // rows with more than 128 entries
-            const int k = kb + lane;
-            const int dv = k < K ? tidx[(int64_t)tl * K + k] - m0 : -1;
-            uint64_t mask = __ballot((unsigned)dv < (unsigned)kTile);
-            while (mask) {
-              const int src = __builtin_ctzll(mask);
-              mask &= mask - 1;
-              const int dvh = __builtin_amdgcn_readlane(dv, src);
-              const float ph = tp[(int64_t)tl * K + kb + src];
-              const int owner = dvh >> 2, comp = dvh & 3;
-              const float zc = comp == 0 ? z[0] : comp == 1 ? z[1] : comp == 2 ? z[2] : z[3];
-              cpart += ph * __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, zc), owner));
-              const float d = lane == owner ? cf * ph : 0.f;
-              if (comp == 0) G[0] -= d;
-              else if (comp == 1) G[1] -= d;
-              else if (comp == 2) G[2] -= d;
-              else G[3] -= d;
-            }
-          }
-          if (lane == 0) part_C[(int64_t)tl * nVT + mt] = cpart;
-          if (dZ != nullptr) {
-            T* dst = dZ + (int64_t)tl * ldz + m0 + vl0;
-            if constexpr (sizeof(T) == 2) {
-              u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
-              *reinterpret_cast<u32x2_t*>(dst) = pk2;
-            } else {
-              *reinterpret_cast<f32x4_t*>(dst) = G;
-            }
-          }
+        T* dst = dZ + (int64_t)(n0 + tl) * ldz + m0 + vl0;
+        if constexpr (sizeof(T) == 2) {
+          u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
+          *reinterpret_cast<u32x2_t*>(dst) = pk2;
+        } else {
+          *reinterpret_cast<f32x4_t*>(dst) = G;
         }
       }
     }
@@ -333,21 +395,23 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   }
 }
 
-// l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2), 0 on ignored rows; per-block
-// partial sums in a fixed order for the deterministic mean.
-__global__ void k_row_loss(const float* part_C, int nVT, const float* rowL2, const float* rowM,
-                           const float* rowH, const float* rowCoef, int rows, float inv_tau,
-                           float* loss_per_token, float* block_partial) {
+// l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2) with C_t = sum_k p_k z_{t, idx_k},
+// 0 on ignored rows; per-block partial sums in a fixed order for the
+// deterministic mean.
+__global__ void k_row_loss(const float* zhit, const float* p, int K, const float* rowL2,
+                           const float* rowM, const float* rowH, const float* rowCoef, int rows,
+                           float inv_tau, float* loss_per_token, float* block_partial) {
   // 64 rows per block (16 per wave); one fixed-order partial per block
   __shared__ float red[4];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   float acc = 0.f;
   for (int rr = 0; rr < 16; ++rr) {
     const int r = blockIdx.x * 64 + wave * 16 + rr;
     if (r >= rows) break;
-    const float* pc = part_C + (int64_t)r * nVT;
+    const float* zr = zhit + (int64_t)r * K;
+    const float* pr = p + (int64_t)r * K;
     float c = 0.f;
-    for (int j = lane; j < nVT; j += 64) c += pc[j];
+    for (int k = lane; k < K; k += 64) c += pr[k] * zr[k];
     c = wave_sum(c);
     const float l = rowCoef[r] != 0.f ? rowH[r] - c * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
     if (lane == 0) {
@@ -399,7 +463,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
                KmOp{reinterpret_cast<const char*>(W + n0),
                     (int64_t)V * ldb - (int64_t)n0 * eb, ldb},
                kb, ke, lds, acc);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -456,7 +520,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, in
   // its rows (rows past V are out of range: loads give 0, stores are dropped);
   // each 64-value block is loaded in one batch before it is stored, so the
   // memory round trips overlap instead of serialising element by element.
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(gW + (int64_t)m0 * D, (uint32_t)mrows * D * 4u);
 #pragma unroll
@@ -494,7 +558,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, in
 // ------------------------------------------------------------ index check --
 // flag |= 1 if an index is outside [0, V); |= 2 if a row repeats an index.
 __global__ void k_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t r = (int64_t)blockIdx.x * 4 + wave_id();
   const int lane = threadIdx.x & 63;
   if (r >= N) return;
   const int32_t* row = idx + r * K;
@@ -524,12 +588,12 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // ------------------------------------------------- event instrumentation ----
 namespace {
 enum ProfKind {
-  P_COUNT_VALID, P_PROLOGUE, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE, P_DW,
-  P_FINALIZE, P_FILL, P_NKINDS
+  P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
+  P_DW, P_FINALIZE, P_FILL, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
-    "count_valid", "teacher_prologue", "logits_lse", "lse_merge", "dz", "row_loss", "dh",
-    "dh_reduce", "dw", "finalize_loss", "fill"};
+    "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
+    "dh", "dh_reduce", "dw", "finalize_loss", "fill"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -624,6 +688,11 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                      a.rowCoef, a.rowCoefM);
     }
 {
+    ProfScope ps_(P_BUCKET, 0.0, s);
+    hipLaunchKernelGGL(k_bucket, dim3(TNt), dim3(kBucketThreads), 0, s, a.tidx, a.p, a.rows, a.K,
+                       (int)a.V, a.nVT, a.hits, a.hitp, a.hoff, a.zhit);
+    }
+{
     ProfScope ps_(P_LOGITS, gemm_flops, s);
     hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
                      (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT);
@@ -636,12 +705,12 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
 {
     ProfScope ps_(P_DZ, gemm_flops, s);
     hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
-                     a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.tidx, a.p, a.K,
-                     static_cast<T*>(a.dZ), a.ldz, a.part_C, a.nVT);
+                     a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits, a.hitp, a.hoff,
+                     a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz, a.zhit);
     }
 {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
-    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 64)), dim3(256), 0, s, a.part_C, a.nVT,
+    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 64)), dim3(256), 0, s, a.zhit, a.p, a.K,
                      a.rowL2, a.rowM, a.rowH, a.rowCoef, a.rows, a.inv_tau, a.loss_per_token,
                      a.block_partial);
     }

@@ -30,8 +30,12 @@ struct KdChunkArgs {
   // per-chunk workspace
   float* p;                 // [rows, K]
   float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
-  float *part_m, *part_s, *part_C;                   // [rows, nVT]
+  float *part_m, *part_s;                            // [rows, nVT]
   int nVT;
+  uint32_t* hits;           // [cdiv(rows, 256) * 256 * K] teacher entries by vocab tile
+  float* hitp;              // their p
+  int* hoff;                // [cdiv(rows, 256), nVT + 1] bucket offsets
+  float* zhit;              // [rows, K] student logit at each teacher entry
   void* dZ;                 // this chunk's rows of the group's dZ [rows, ldz]
   int64_t ldz;              // = padded vocabulary (columns V..ldz are written as 0)
   int dh_split;

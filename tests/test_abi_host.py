@@ -78,7 +78,7 @@ def test_workspace_size_null(lib):
 
 def test_workspace_linear_not_nv(lib):
     """The workspace is bounded by a constant in N (chunk-sized buffers, a dW
-    group of at most 8192 gathered tokens) plus per-64-row loss partials."""
+    group of at most 16384 gathered tokens) plus per-64-row loss partials."""
     sizes = {}
     for N in (4096, 32768, 262144):
         rc, b = _ws(lib, _prob(N=N, D=4096, V=131072, K=100, chunk=4096, dtype=kd.KD_BF16))
