@@ -386,9 +386,11 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
   // 0's 32 MFMAs run interleaved with the reads of sub-step 1's fragments;
   // then the wave waits for its reads and for step j+1's DMA, the barrier
   // publishes every wave's DMA and retires stage j % S, and sub-step 1's MFMAs
-  // run in 16 pairs, each pair issued with one DMA instruction of step j+S
-  // (into the retired stage) and one fragment of step j+1's sub-step 0. Two
-  // waves per SIMD fill each other's waits.
+  // run in 16 pairs: every other pair is issued with one DMA instruction of
+  // step j+S (into the retired stage; spreading them keeps the LDS writes from
+  // bunching up against the fragment reads), and the first 12 pairs each with
+  // one fragment of step j+1's sub-step 0. Two waves per SIMD fill each
+  // other's waits.
 #pragma unroll
   for (int p = 0; p < S; ++p) {
     char* a = lds + p * STB;
@@ -427,8 +429,10 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
       const DmaStep sb = db.prep(opb, a + OPB, wave, ks, ks < ks_end);
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        if (q < 4) sa.one(q);
-        else if (q < 8) sb.one(q - 4);
+        if ((q & 1) == 0) {
+          if (q < 8) sa.one(q >> 1);
+          else sb.one((q - 8) >> 1);
+        }
         mfma2(q, fa[1], fb[1]);
         if (q < 8) fa[0][q] = fra.one(n, 0, q);
         else if (q < 12) fb[0][q - 8] = frb.one(n + OPB, 0, q - 8);
