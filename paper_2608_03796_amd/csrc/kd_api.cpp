@@ -30,7 +30,7 @@ struct Plan {
   int64_t Vp;          // V rounded up to the 256-column tile
   int64_t nVT;         // vocabulary tiles
   int64_t nchunks;
-  int64_t nblk;        // loss partials of a full chunk (one per 64 rows)
+  int64_t nblk;        // loss partials of a full chunk (one per 16 rows)
   int64_t G;           // chunks whose dZ rows are gathered before one dW GEMM
   int dh_split;
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
@@ -79,7 +79,7 @@ Plan make_plan(const kd_problem* p) {
   pl.Vp = rup(pl.V, kTile);
   pl.nVT = pl.Vp / kTile;
   pl.nchunks = cdiv(pl.N, pl.c);
-  pl.nblk = cdiv(pl.c, 64);
+  pl.nblk = cdiv(pl.c, 16);
   // dW is accumulated in fp32 in place: each dW GEMM reads and writes all of
   // grad_W once, so gather the dZ rows of up to ~16384 tokens (and at most
   // 4 GiB of dZ) per GEMM
@@ -219,7 +219,7 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     a.block_partial = lossp + n_partials;
     a.gH = want_dh ? static_cast<char*>(grad_hidden) + row0 * pl.D * pl.eb : nullptr;
     if (kd_launch_chunk(&a, hip_stream) != 0) return KD_ERR_DEVICE;
-    n_partials += cdiv(rcount, 64);
+    n_partials += cdiv(rcount, 16);
     group_tokens += rcount;
     if (want_dw && (slot == pl.G - 1 || ci == pl.nchunks - 1)) {
       KdDwArgs d{};

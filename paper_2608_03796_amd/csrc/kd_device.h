@@ -88,18 +88,34 @@ __device__ __forceinline__ f32x4_t mfma_slot(u32x4_t a, u32x4_t b, f32x4_t c, fl
   return c;
 }
 
-// Accumulator layout of wave w (wm = w >> 2 in 0..1, wn = w & 3 in 0..3)
-// after gemm_tile: acc.v[i][j][r] (i < 8, j < 4, r < 4) is C[m][n] with
+// A 256x256 tile is computed by NW waves: 8 waves in a 2 (M) x 4 (N) grid,
+// each 128x64, or 4 waves in a 2 x 2 grid, each 128x128 (its accumulators
+// then live in the AGPR half of the register file). Accumulator layout of wave
+// w (wm = w / (NW/2), wn = w % (NW/2)) after gemm_tile: acc.v[i][j][r]
+// (i < 8, j < NJ, r < 4) is C[m][n] with
 //   m = wm*128 + 16*i + 4*(lane>>4) + r
-//   n = wn*64 + 16*j + (lane&15)
+//   n = wn*16*NJ + 16*j + (lane&15)
 // (the 16x16 MFMA output layout: lane holds column lane&15 of 4 rows).
-struct AccTile {
-  f32x4_t v[8][4];
+template <int NW>
+struct WaveGrid {
+  static_assert(NW == 8 || NW == 4, "8 or 4 waves per 256x256 tile");
+  static constexpr int NJ = 32 / NW;         // 16-column blocks per wave
+  static constexpr int NPW = 32 / NW;        // DMA instructions per wave per operand step
+  __device__ static int wm(int wave) { return wave >> (NW == 8 ? 2 : 1); }
+  __device__ static int wn(int wave) { return wave & (NW / 2 - 1); }
 };
+template <int NJ>
+struct AccTileT {
+  f32x4_t v[8][NJ];
+};
+typedef AccTileT<4> AccTile;  // 8-wave tiles
 __device__ __forceinline__ int acc_m(int wm, int i, int lane, int r) {
   return wm * 128 + 16 * i + 4 * (lane >> 4) + r;
 }
-__device__ __forceinline__ int acc_n(int wn, int j, int lane) { return wn * 64 + 16 * j + (lane & 15); }
+template <int NJ = 4>
+__device__ __forceinline__ int acc_n(int wn, int j, int lane) {
+  return wn * 16 * NJ + 16 * j + (lane & 15);
+}
 
 // One 256x256 output tile: acc = A[m0:m0+256, k-range] * B[n0:n0+256, k-range]^T.
 //
@@ -193,69 +209,72 @@ __device__ __forceinline__ uint32_t lds_addr(const char* p) {
 // DMA of one operand's K step: 4 instructions of 1 KiB per wave. prep()
 // computes the step's resource, LDS address and offsets; one(i) issues
 // instruction i.
+template <int NPW>
 struct DmaStep {
   i32x4_t r;
   uint32_t la;
-  uint32_t off[4];
+  uint32_t off[NPW];
   __device__ __forceinline__ void one(int i) const { dma_b128(r, la + i * 1024, off[i]); }
 };
 
-template <typename T, typename Op>
+// An operand's 32 KiB stage is 32 instructions of 1 KiB; wave w issues
+// instructions w*NPW .. w*NPW + NPW - 1.
+template <typename T, typename Op, int NPW>
 struct OpDma;
 
-template <typename T>
-struct OpDma<T, KcOp> {
-  uint32_t voff[4];
+template <typename T, int NPW>
+struct OpDma<T, KcOp, NPW> {
+  uint32_t voff[NPW];
   i32x4_t r;
   __device__ __forceinline__ void init(const KcOp& op, int wave, int lane) {
     r = rsrc_words(op.base, op.bytes);
     // 8 rows of 128 bytes per instruction: lane -> row 8q + lane/8, slot lane%8
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = (wave * 4 + i) * 8 + (lane >> 3);
+    for (int i = 0; i < NPW; ++i) {
+      const int row = (wave * NPW + i) * 8 + (lane >> 3);
       voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)(((lane & 7) ^ swz_kc(row)) << 4);
     }
   }
-  __device__ __forceinline__ DmaStep prep(const KcOp&, char* stage, int wave, int ks,
-                                          bool live) const {
-    DmaStep d;
+  __device__ __forceinline__ DmaStep<NPW> prep(const KcOp&, char* stage, int wave, int ks,
+                                               bool live) const {
+    DmaStep<NPW> d;
     d.r = r;
-    d.la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
+    d.la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * NPW * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NPW; ++i)
       d.off[i] = live ? voff[i] + (uint32_t)ks * (uint32_t)kRowB : kOobOffset;
     return d;
   }
 };
 
-template <typename T>
-struct OpDma<T, KmOp> {
+template <typename T, int NPW>
+struct OpDma<T, KmOp, NPW> {
   static constexpr int KS = kRowB / (int)sizeof(T);  // K rows per step
-  uint32_t voff[4];
+  uint32_t voff[NPW];
   __device__ __forceinline__ void init(const KmOp& op, int wave, int lane) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NPW; ++i) {
       if constexpr (sizeof(T) == 2) {
         // 2 K rows of 512 bytes per instruction: lane -> row 2q + lane/32, slot lane%32
-        const int row = (wave * 4 + i) * 2 + (lane >> 5);
+        const int row = (wave * NPW + i) * 2 + (lane >> 5);
         voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)(((lane & 31) ^ swz_km16(row)) << 4);
       } else {
         // 1 K row of 1 KiB per instruction: lane -> slot lane
-        const int row = wave * 4 + i;
+        const int row = wave * NPW + i;
         voff[i] = (uint32_t)row * (uint32_t)op.ld + (uint32_t)((lane ^ swz_km32(row)) << 4);
       }
     }
   }
-  __device__ __forceinline__ DmaStep prep(const KmOp& op, char* stage, int wave, int ks,
-                                          bool live) const {
+  __device__ __forceinline__ DmaStep<NPW> prep(const KmOp& op, char* stage, int wave, int ks,
+                                               bool live) const {
     const int64_t step0 = (int64_t)ks * KS * op.ld;
     int64_t left = op.bytes - step0;
     left = left < 0 ? 0 : (left > 0x7fffffff ? 0x7fffffff : left);
-    DmaStep d;
+    DmaStep<NPW> d;
     d.r = rsrc_words(op.base + step0, (uint32_t)left);
-    d.la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * 4096);
+    d.la = __builtin_amdgcn_readfirstlane(lds_addr(stage) + wave * NPW * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) d.off[i] = live ? voff[i] : kOobOffset;
+    for (int i = 0; i < NPW; ++i) d.off[i] = live ? voff[i] : kOobOffset;
     return d;
   }
 };
@@ -333,26 +352,30 @@ struct OpFrag<float, KmOp, NB> {
   }
 };
 
-template <typename T, typename OA, typename OB>
+template <typename T, typename OA, typename OB, int NW = 8>
 __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_begin, int ks_end,
-                                          char* lds, AccTile& acc) {
+                                          char* lds, AccTileT<WaveGrid<NW>::NJ>& acc) {
+  typedef WaveGrid<NW> WG;
+  constexpr int NJ = WG::NJ, NPW = WG::NPW;
   constexpr int S = kStages;
   constexpr int OPB = kTile * kRowB;  // one operand's stage (32 KiB)
   constexpr int STB = 2 * OPB;        // one stage (A and B)
-  constexpr int NI = 8;               // DMA instructions per K step per wave
-  constexpr int RD = OpFrag<T, OA, 8>::kReads + OpFrag<T, OB, 4>::kReads;
-  constexpr int RQ = (RD + 15) / 16;  // LDS reads per MFMA pair in sub-step 0
+  constexpr int NI = 2 * NPW;         // DMA instructions per K step per wave
+  constexpr int NP = 4 * NJ;          // MFMA pairs per sub-step
+  constexpr int RD = OpFrag<T, OA, 8>::kReads + OpFrag<T, OB, NJ>::kReads;
+  constexpr int RQ = (RD + NP - 1) / NP;  // LDS reads per MFMA pair in sub-step 0
   static_assert((S - 1) * NI <= 63, "vmcnt range of the in-flight DMA steps");
+  static_assert(2 * NI == NP, "one DMA instruction on every other MFMA pair");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = wave_id();
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = WG::wm(wave), wn = WG::wn(wave);
 
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc.v[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NJ; ++j) acc.v[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nsteps = ks_end - ks_begin;
   if (nsteps <= 0) {
@@ -360,59 +383,58 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
     return;
   }
 
-  OpDma<T, OA> da;
-  OpDma<T, OB> db;
+  OpDma<T, OA, NPW> da;
+  OpDma<T, OB, NPW> db;
   da.init(opa, wave, lane);
   db.init(opb, wave, lane);
   OpFrag<T, OA, 8> fra;
-  OpFrag<T, OB, 4> frb;
+  OpFrag<T, OB, NJ> frb;
   fra.init(wm * 128, lane);
-  frb.init(wn * 64, lane);
+  frb.init(wn * 16 * NJ, lane);
 
-  auto frag = [&](int stage, int s, u32x4_t (&fa)[8], u32x4_t (&fb)[4]) {
+  auto frag = [&](int stage, int s, u32x4_t (&fa)[8], u32x4_t (&fb)[NJ]) {
     const char* a = lds + stage * STB;
 #pragma unroll
     for (int b = 0; b < 8; ++b) fa[b] = fra.one(a, s, b);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) fb[b] = frb.one(a + OPB, s, b);
+    for (int b = 0; b < NJ; ++b) fb[b] = frb.one(a + OPB, s, b);
   };
-  auto mfma2 = [&](int q, const u32x4_t (&fa)[8], const u32x4_t (&fb)[4]) {
-    const int i = q >> 1, j = 2 * (q & 1);
+  auto mfma2 = [&](int q, const u32x4_t (&fa)[8], const u32x4_t (&fb)[NJ]) {
+    const int i = q / (NJ / 2), j = 2 * (q % (NJ / 2));
     acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
     acc.v[i][j + 1] = mfma_slot(fa[i], fb[j + 1], acc.v[i][j + 1], (T*)nullptr);
   };
 
   // Step j lives in stage j % S; S steps of DMA are always in flight. Sub-step
-  // 0's 32 MFMAs run interleaved with the reads of sub-step 1's fragments;
-  // then the wave waits for its reads and for step j+1's DMA, the barrier
+  // 0's MFMAs run interleaved with the reads of sub-step 1's fragments; then
+  // the wave waits for its reads and for step j+1's DMA, the barrier
   // publishes every wave's DMA and retires stage j % S, and sub-step 1's MFMAs
-  // run in 16 pairs: every other pair is issued with one DMA instruction of
-  // step j+S (into the retired stage; spreading them keeps the LDS writes from
-  // bunching up against the fragment reads), and the first 12 pairs each with
-  // one fragment of step j+1's sub-step 0. Two waves per SIMD fill each
-  // other's waits.
+  // run in pairs: every other pair is issued with one DMA instruction of step
+  // j+S (into the retired stage; spreading them keeps the LDS writes from
+  // bunching up against the fragment reads), and the first 8 + NJ pairs each
+  // with one fragment of step j+1's sub-step 0.
 #pragma unroll
   for (int p = 0; p < S; ++p) {
     char* a = lds + p * STB;
     const bool live = ks_begin + p < ks_end;
-    const DmaStep sa = da.prep(opa, a, wave, ks_begin + p, live);
-    const DmaStep sb = db.prep(opb, a + OPB, wave, ks_begin + p, live);
+    const DmaStep<NPW> sa = da.prep(opa, a, wave, ks_begin + p, live);
+    const DmaStep<NPW> sb = db.prep(opb, a + OPB, wave, ks_begin + p, live);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sa.one(i);
+    for (int i = 0; i < NPW; ++i) sa.one(i);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sb.one(i);
+    for (int i = 0; i < NPW; ++i) sb.one(i);
   }
   KD_VMCNT((S - 1) * NI);
   __syncthreads();
-  u32x4_t fa[2][8], fb[2][4];
+  u32x4_t fa[2][8], fb[2][NJ];
   frag(0, 0, fa[0], fb[0]);
   int st = 0;
   for (int j = 0; j < nsteps; ++j) {
     frag(st, 1, fa[1], fb[1]);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) mfma2(q, fa[0], fb[0]);
+    for (int q = 0; q < NP; ++q) mfma2(q, fa[0], fb[0]);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
+    for (int q = 0; q < NP; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, RQ, 0);  // LDS read
     }
@@ -425,17 +447,17 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
       char* a = lds + st * STB;
       const char* n = lds + nst * STB;
       const int ks = ks_begin + j + S;
-      const DmaStep sa = da.prep(opa, a, wave, ks, ks < ks_end);
-      const DmaStep sb = db.prep(opb, a + OPB, wave, ks, ks < ks_end);
+      const DmaStep<NPW> sa = da.prep(opa, a, wave, ks, ks < ks_end);
+      const DmaStep<NPW> sb = db.prep(opb, a + OPB, wave, ks, ks < ks_end);
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
+      for (int q = 0; q < NP; ++q) {
         if ((q & 1) == 0) {
-          if (q < 8) sa.one(q >> 1);
-          else sb.one((q - 8) >> 1);
+          if (q < 2 * NPW) sa.one(q >> 1);
+          else sb.one((q - 2 * NPW) >> 1);
         }
         mfma2(q, fa[1], fb[1]);
         if (q < 8) fa[0][q] = fra.one(n, 0, q);
-        else if (q < 12) fb[0][q - 8] = frb.one(n + OPB, 0, q - 8);
+        else if (q < 8 + NJ) fb[0][q - 8] = frb.one(n + OPB, 0, q - 8);
         __builtin_amdgcn_sched_barrier(0);
       }
     }

@@ -192,7 +192,8 @@ __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, 
 // with their teacher probability in `hitp`. An index outside [0, V) gets no
 // slot and a zero z (it contributes nothing to C or dZ).
 constexpr int kBucketThreads = 1024;
-constexpr int kMaxVT = 4096;  // vocabulary tiles (V <= 2^20)
+constexpr int kBucketBatch = 8;  // entries per thread whose loads are in flight together
+constexpr int kMaxVT = 4096;     // vocabulary tiles (V <= 2^20)
 
 __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __restrict__ tidx,
                                                            const float* __restrict__ p, int rows,
@@ -205,16 +206,27 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __rest
   const int t0 = blockIdx.x * kTile;
   const int total = min(kTile, rows - t0) * K;
   const int64_t seg = (int64_t)blockIdx.x * kTile * K;
+  // entry e of the tile is element t0 K + e of the row-major [rows, K] arrays
+  const int32_t* ti = tidx + (int64_t)t0 * K;
+  const float invK = 1.0f / (float)K;
   for (int b = tid; b < nVT; b += kBucketThreads) cnt[b] = 0;
   __syncthreads();
-  for (int e = tid; e < total; e += kBucketThreads) {
-    const int tl = e / K, k = e - tl * K;
-    const int64_t g = (int64_t)(t0 + tl) * K + k;
-    const int v = tidx[g];
-    if ((unsigned)v < (unsigned)V)
-      atomicAdd(&cnt[v >> 8], 1);
-    else
-      zhit[g] = 0.f;
+  for (int base = 0; base < total; base += kBucketThreads * kBucketBatch) {
+    int v[kBucketBatch];
+#pragma unroll
+    for (int u = 0; u < kBucketBatch; ++u) {
+      const int e = base + u * kBucketThreads + tid;
+      v[u] = e < total ? ti[e] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kBucketBatch; ++u) {
+      const int e = base + u * kBucketThreads + tid;
+      if (e >= total) continue;
+      if ((unsigned)v[u] < (unsigned)V)
+        atomicAdd(&cnt[v[u] >> 8], 1);
+      else
+        zhit[(int64_t)t0 * K + e] = 0.f;
+    }
   }
   __syncthreads();
   // exclusive scan: thread tid owns bins [tid R, tid R + R)
@@ -245,14 +257,26 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __rest
   }
   if (tid == kBucketThreads - 1) ho[nVT] = off;
   __syncthreads();
-  for (int e = tid; e < total; e += kBucketThreads) {
-    const int tl = e / K, k = e - tl * K;
-    const int64_t g = (int64_t)(t0 + tl) * K + k;
-    const int v = tidx[g];
-    if ((unsigned)v < (unsigned)V) {
-      const int pos = atomicAdd(&cur[v >> 8], 1);
-      hits[seg + pos] = (uint32_t)tl | ((uint32_t)(v & 255) << 8) | ((uint32_t)k << 16);
-      hitp[seg + pos] = p[g];
+  for (int base = 0; base < total; base += kBucketThreads * kBucketBatch) {
+    int v[kBucketBatch];
+    float pv[kBucketBatch];
+#pragma unroll
+    for (int u = 0; u < kBucketBatch; ++u) {
+      const int e = base + u * kBucketThreads + tid;
+      v[u] = e < total ? ti[e] : -1;
+      pv[u] = e < total ? p[(int64_t)t0 * K + e] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBucketBatch; ++u) {
+      const int e = base + u * kBucketThreads + tid;
+      if (e >= total || (unsigned)v[u] >= (unsigned)V) continue;
+      // token = e / K (exact: e < 2^20, and (e + 0.5) / K stays >= 1/(2K)
+      // away from an integer while the float product errs by < 2^-12)
+      const int tl = (int)(((float)e + 0.5f) * invK);
+      const int k = e - tl * K;
+      const int pos = atomicAdd(&cur[v[u] >> 8], 1);
+      hits[seg + pos] = (uint32_t)tl | ((uint32_t)(v[u] & 255) << 8) | ((uint32_t)k << 16);
+      hitp[seg + pos] = pv[u];
     }
   }
 }
@@ -398,22 +422,28 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
 // l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2) with C_t = sum_k p_k z_{t, idx_k},
 // 0 on ignored rows; per-block partial sums in a fixed order for the
 // deterministic mean.
+constexpr int kLossRows = 16;  // rows per row-loss block (4 per wave)
 __global__ void k_row_loss(const float* zhit, const float* p, int K, const float* rowL2,
                            const float* rowM, const float* rowH, const float* rowCoef, int rows,
                            float inv_tau, float* loss_per_token, float* block_partial) {
-  // 64 rows per block (16 per wave); one fixed-order partial per block
+  // one fixed-order partial per block
   __shared__ float red[4];
   const int lane = threadIdx.x & 63, wave = wave_id();
+  float c[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k = lane; k < K; k += 64) {
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int r = blockIdx.x * kLossRows + wave * 4 + rr;
+      if (r < rows) c[rr] += p[(int64_t)r * K + k] * zhit[(int64_t)r * K + k];
+    }
+  }
   float acc = 0.f;
-  for (int rr = 0; rr < 16; ++rr) {
-    const int r = blockIdx.x * 64 + wave * 16 + rr;
-    if (r >= rows) break;
-    const float* zr = zhit + (int64_t)r * K;
-    const float* pr = p + (int64_t)r * K;
-    float c = 0.f;
-    for (int k = lane; k < K; k += 64) c += pr[k] * zr[k];
-    c = wave_sum(c);
-    const float l = rowCoef[r] != 0.f ? rowH[r] - c * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
+#pragma unroll
+  for (int rr = 0; rr < 4; ++rr) {
+    const int r = blockIdx.x * kLossRows + wave * 4 + rr;
+    const float cs = wave_sum(c[rr]);
+    if (r >= rows) continue;
+    const float l = rowCoef[r] != 0.f ? rowH[r] - cs * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
     if (lane == 0) {
       if (loss_per_token) loss_per_token[r] = l;
       acc += l;
@@ -710,7 +740,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     }
 {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
-    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, 64)), dim3(256), 0, s, a.zhit, a.p, a.K,
+    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(256), 0, s, a.zhit, a.p, a.K,
                      a.rowL2, a.rowM, a.rowH, a.rowCoef, a.rows, a.inv_tau, a.loss_per_token,
                      a.block_partial);
     }

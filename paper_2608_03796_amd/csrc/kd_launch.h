@@ -42,7 +42,7 @@ struct KdChunkArgs {
   float* dh_partial;        // [dh_split, rows, D] when dh_split > 1
   // outputs
   float* loss_per_token;    // + row0, or null
-  float* block_partial;     // this chunk's cdiv(rows, 64) partial sums
+  float* block_partial;     // this chunk's cdiv(rows, 16) partial sums
   void* gH;                 // grad_hidden + row0 * D, or null
 };
 
