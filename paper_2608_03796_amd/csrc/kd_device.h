@@ -352,7 +352,12 @@ struct OpFrag<float, KmOp, NB> {
   }
 };
 
-template <typename T, typename OA, typename OB, int NW = 8>
+// SPREAD selects the fragment-read placement: false puts sub-step 1's reads
+// under the compiler's MFMA/read interleave and sub-step 0's reads on the
+// first pairs of the second half; true places both by hand, fragment f with
+// pair f * NP / (8 + NJ). Which one is faster depends on the operand layouts
+// (measured per kernel).
+template <typename T, typename OA, typename OB, int NW = 8, bool SPREAD = false>
 __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_begin, int ks_end,
                                           char* lds, AccTileT<WaveGrid<NW>::NJ>& acc) {
   typedef WaveGrid<NW> WG;
@@ -411,8 +416,8 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
   // publishes every wave's DMA and retires stage j % S, and sub-step 1's MFMAs
   // run in pairs: every other pair is issued with one DMA instruction of step
   // j+S (into the retired stage; spreading them keeps the LDS writes from
-  // bunching up against the fragment reads), and the first 8 + NJ pairs each
-  // with one fragment of step j+1's sub-step 0.
+  // bunching up against the fragment reads), and the fragments of step j+1's
+  // sub-step 0 are read alongside (placement per SPREAD).
 #pragma unroll
   for (int p = 0; p < S; ++p) {
     char* a = lds + p * STB;
@@ -429,16 +434,35 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
   u32x4_t fa[2][8], fb[2][NJ];
   frag(0, 0, fa[0], fb[0]);
   int st = 0;
+  constexpr int NF = 8 + NJ;  // fragments per sub-step
+  auto read_at = [&](int q, const char* a, int s, u32x4_t (&xa)[8], u32x4_t (&xb)[NJ]) {
+#pragma unroll
+    for (int f = 0; f < NF; ++f)
+      if ((SPREAD ? (f * NP) / NF : f) == q) {
+        if (f < 8) xa[f] = fra.one(a, s, f);
+        else xb[f - 8] = frb.one(a + OPB, s, f - 8);
+      }
+  };
   for (int j = 0; j < nsteps; ++j) {
-    frag(st, 1, fa[1], fb[1]);
+    if constexpr (SPREAD) {
+      const char* c = lds + st * STB;
 #pragma unroll
-    for (int q = 0; q < NP; ++q) mfma2(q, fa[0], fb[0]);
+      for (int q = 0; q < NP; ++q) {
+        mfma2(q, fa[0], fb[0]);
+        read_at(q, c, 1, fa[1], fb[1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      frag(st, 1, fa[1], fb[1]);
 #pragma unroll
-    for (int q = 0; q < NP; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, RQ, 0);  // LDS read
+      for (int q = 0; q < NP; ++q) mfma2(q, fa[0], fb[0]);
+#pragma unroll
+      for (int q = 0; q < NP; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, RQ, 0);  // LDS read
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xc07f & ~0x0f00);  // lgkmcnt(0)
     KD_VMCNT((S - 2) * NI);
     __syncthreads();
@@ -456,8 +480,12 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
           else sb.one((q - 2 * NPW) >> 1);
         }
         mfma2(q, fa[1], fb[1]);
-        if (q < 8) fa[0][q] = fra.one(n, 0, q);
-        else if (q < 8 + NJ) fb[0][q - 8] = frb.one(n + OPB, 0, q - 8);
+        if constexpr (SPREAD) {
+          read_at(q, n, 0, fa[0], fb[0]);
+        } else {
+          if (q < 8) fa[0][q] = fra.one(n, 0, q);
+          else if (q < 8 + NJ) fb[0][q - 8] = frb.one(n + OPB, 0, q - 8);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     }

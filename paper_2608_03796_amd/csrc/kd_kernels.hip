@@ -489,7 +489,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const int kb = sidx * per, ke = min(ks_total, kb + per);
   AccTile acc;
   const int mrows = min(kTile, rows - m0);
-  gemm_tile<T>(KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
+  gemm_tile<T, KcOp, KmOp, 8, true>(
+      KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
                KmOp{reinterpret_cast<const char*>(W + n0),
                     (int64_t)V * ldb - (int64_t)n0 * eb, ldb},
                kb, ke, lds, acc);
@@ -546,42 +547,62 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, in
   gemm_tile<T>(KmOp{reinterpret_cast<const char*>(dZ + m0), (int64_t)tokens * lda - (int64_t)m0 * eb, lda},
                KmOp{reinterpret_cast<const char*>(Hg + n0), (int64_t)tokens * ldb - (int64_t)n0 * eb, ldb},
                0, (tokens + KS - 1) / KS, lds, acc);
-  // fp32 read-modify-write of the output tile through a buffer resource over
-  // its rows (rows past V are out of range: loads give 0, stores are dropped);
-  // each 64-value block is loaded in one batch before it is stored, so the
-  // memory round trips overlap instead of serialising element by element.
+  // Output tile in two halves of 128 rows: the waves holding a half stage it
+  // in LDS (fp32, 16-float column groups XOR-swizzled by row so the staging
+  // writes of a wave's 4 row groups hit distinct banks), then every thread
+  // moves 16-byte row pieces: with beta = 1 all of its old values are loaded
+  // before any store of the half, then added and stored. Rows past V and
+  // columns past D are skipped.
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
-  const __amdgpu_buffer_rsrc_t ro = make_rsrc(gW + (int64_t)m0 * D, (uint32_t)mrows * D * 4u);
+  const int tid = threadIdx.x;
+  float* stg = reinterpret_cast<float*>(lds);  // [128][256]
+  const int ncols = min(kTile, D - n0);
 #pragma unroll
-  for (int ib = 0; ib < 8; ib += 2) {
-    float old[2][4][4];
+  for (int h = 0; h < 2; ++h) {
+    if (wm == h) {
 #pragma unroll
-    for (int di = 0; di < 2; ++di)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const uint32_t row = (uint32_t)acc_m(wm, ib + di, lane, r);
-          const uint32_t col = (uint32_t)(n0 + acc_n(wn, j, lane));  // base is column 0
-          old[di][j][r] = 0.f;
-          if (beta && (int)col < D)
-            old[di][j][r] = __builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(ro, (int)((row * (uint32_t)D + col) * 4u), 0, 0));
-        }
+          for (int r = 0; r < 4; ++r) {
+            const int row = acc_m(0, i, lane, r);
+            const int col = acc_n(wn, j, lane) ^ (((row >> 2) & 3) << 4);
+            stg[row * 256 + col] = acc.v[i][j][r];
+          }
+    }
+    __syncthreads();
+    // rows of this half as one buffer resource: rows past V are out of
+    // range, columns past D get an out-of-range offset (loads give 0, stores
+    // are dropped), so no lane branches and no load waits behind a store
+    const int hrows = __builtin_amdgcn_readfirstlane(max(0, min(128, mrows - 128 * h)));
+    const __amdgpu_buffer_rsrc_t ro =
+        make_rsrc(gW + (int64_t)(m0 + 128 * h) * D, (uint32_t)hrows * (uint32_t)D * 4u);
+    uint32_t off[16];
 #pragma unroll
-    for (int di = 0; di < 2; ++di)
+    for (int u = 0; u < 16; ++u) {
+      const int q = tid + kThreads * u;
+      const int row = q >> 6, c4 = (q & 63) * 4;
+      off[u] = c4 < ncols ? ((uint32_t)row * (uint32_t)D + (uint32_t)(n0 + c4)) * 4u : kOobOffset;
+    }
+    u32x4_t old[16];
+    if (beta) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int u = 0; u < 16; ++u) old[u] = __builtin_amdgcn_raw_buffer_load_b128(ro, off[u], 0, 0);
+    } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const uint32_t row = (uint32_t)acc_m(wm, ib + di, lane, r);
-          const uint32_t col = (uint32_t)(n0 + acc_n(wn, j, lane));
-          if ((int)col < D)
-            __builtin_amdgcn_raw_buffer_store_b32(
-                __builtin_bit_cast(uint32_t, old[di][j][r] + acc.v[ib + di][j][r]), ro,
-                (int)((row * (uint32_t)D + col) * 4u), 0, 0);
-        }
+      for (int u = 0; u < 16; ++u) old[u] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int q = tid + kThreads * u;
+      const int row = q >> 6, c4 = (q & 63) * 4;
+      const f32x4_t v = *reinterpret_cast<const f32x4_t*>(stg + row * 256 + (c4 ^ (((row >> 2) & 3) << 4)));
+      const f32x4_t o = __builtin_bit_cast(f32x4_t, old[u]);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, o + v), ro, off[u], 0, 0);
+    }
+    __syncthreads();
   }
 }
 
