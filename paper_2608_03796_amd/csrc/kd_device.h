@@ -159,10 +159,15 @@ struct KmOp {
   int ld;  // row pitch in bytes
 };
 
-// 16-byte slot swizzles, chosen so the DMA rows and every 32-lane half of a
-// fragment read touch all 64 LDS banks once.
-// K-contiguous rows: 8 slots of 128 bytes.
-__device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
+// 16-byte slot swizzles of the LDS stages. The DMA writes whole 1 KiB runs
+// (conflict-free for any permutation); the swizzles make the fragment reads
+// conflict-free. The K-contiguous pattern was chosen by measurement
+// (SQ_LDS_BANK_CONFLICT and read throughput of the exact fragment-read
+// pattern): XOR of the slot with row % 8 reads at full rate, while
+// (row ^ row/8) % 8, which a 16-consecutive-lane bank model also predicts to
+// be conflict-free, measured 2-way.
+// K-contiguous rows: 128 bytes, 8 slots.
+__device__ __forceinline__ int swz_kc(int row) { return row & 7; }
 // K-major bf16 rows (512 bytes, 32 slots): a transposing read covers slot
 // pairs of rows r..r+3 and r+8..r+11, which get 8 distinct even XOR values.
 __device__ __forceinline__ int swz_km16(int row) {
