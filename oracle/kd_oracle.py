@@ -18,7 +18,12 @@ Fused Chunked KL Loss". What this module computes, and from which passage:
   §3.2.1, which the paper names its correctness baseline. The GPU path instead
   evaluates the decomposition of Eq. (2); agreement therefore also checks the
   Eq. (1) = Eq. (2) identity.
-* The mean over loss-masked (non-ignored) positions (§3, after Eq. 1).
+* The mean over loss-masked (non-ignored) positions (§3, after Eq. 1); or, for
+  the backward of Algorithm 1 driven by an upstream gradient, any per-token
+  weights g_t of the token losses.
+* The partial-mass teacher of §3.2: cached top-K probabilities with retained
+  mass M = sum_k p_k <= 1, supplied as log-probabilities and used as they are
+  (no renormalisation, no temperature).
 * Gradients from the closed form of Eq. (3) in §3.2.3, dL/dz_v = M q_v - p_v,
   taken through the temperature (the 1/tau chain factor) and the mean weight
   g_t = 1/N_valid, then projected back as in Algorithm 1's backward:
@@ -49,25 +54,37 @@ def log_softmax_rows(y):
     return y - (m + np.log(np.exp(y - m).sum(axis=1, keepdims=True)))
 
 
-def teacher_distribution(teacher_logit, tau):
-    """Support probabilities p[N, K] = softmax over the K cached entries of
-    teacher_logit / tau (§3.2, offline top-K teacher)."""
-    return np.exp(log_softmax_rows(_f64(teacher_logit) / float(tau)))
+def teacher_distribution(teacher_logit, tau, mode="logits"):
+    """Support probabilities p[N, K] of the offline top-K teacher (§3.2).
+
+    mode "logits": softmax over the K cached entries of teacher_logit / tau
+    (retained mass 1). mode "logprobs": the cached values are the teacher's
+    log-probabilities over the full vocabulary, p = exp(value), retained mass
+    M = sum_k p_k <= 1 (the partial-mass teacher)."""
+    if mode == "logits":
+        return np.exp(log_softmax_rows(_f64(teacher_logit) / float(tau)))
+    if mode == "logprobs":
+        return np.exp(_f64(teacher_logit))
+    raise ValueError("mode must be 'logits' or 'logprobs'")
 
 
 def kd_topk_kl(h, W, teacher_idx, teacher_logit, tau=1.0, ignore=None,
-               chunk=None, mean_denominator=None, want_grads=True):
+               chunk=None, mean_denominator=None, want_grads=True,
+               token_weights=None, teacher_mode="logits"):
     """Loss, per-token loss, log-normaliser and gradients of the top-K forward KL.
 
     h [N, D], W [V, D] (any real dtype; computed in float64),
     teacher_idx [N, K] ints in [0, V), teacher_logit [N, K], ignore [N] (nonzero =
     excluded) or None, chunk = rows per chunk (None = all rows at once),
     mean_denominator = divisor of the mean (None = number of non-ignored rows;
-    a caller checking a subset of a bigger batch passes the batch's count).
+    a caller checking a subset of a bigger batch passes the batch's count),
+    token_weights [N] = weight g_t of each token's loss in the differentiated
+    objective sum_t g_t l_t (None = the mean's 1/N_valid; ignored rows always 0),
+    teacher_mode = "logits" or "logprobs" (see teacher_distribution).
 
-    Returns a dict with: loss (float), loss_per_token [N] (0 on ignored rows),
-    logZ [N] (log-normaliser of z/tau), M [N], and when want_grads:
-    grad_hidden [N, D], grad_W [V, D].
+    Returns a dict with: loss (float, the mean), loss_per_token [N] (0 on ignored
+    rows), logZ [N] (log-normaliser of z/tau), M [N], and when want_grads the
+    gradients of the objective: grad_hidden [N, D], grad_W [V, D].
     """
     h = _f64(h)
     W = _f64(W)
@@ -84,10 +101,14 @@ def kd_topk_kl(h, W, teacher_idx, teacher_logit, tau=1.0, ignore=None,
     if c <= 0:
         raise ValueError("chunk must be positive")
 
-    p = teacher_distribution(teacher_logit, tau) if K > 0 else np.zeros((N, 0))
+    p = teacher_distribution(teacher_logit, tau, teacher_mode) if K > 0 else np.zeros((N, 0))
     M = p.sum(axis=1)
-    # weight of each token in the mean (§3: averaged over loss-masked positions)
-    g = np.where(valid, 1.0 / n_valid, 0.0) if n_valid > 0 else np.zeros(N)
+    # weight of each token in the objective: the mean's 1/N_valid over the
+    # loss-masked positions (§3), or the caller's upstream per-token weights
+    if token_weights is None:
+        g = np.where(valid, 1.0 / n_valid, 0.0) if n_valid > 0 else np.zeros(N)
+    else:
+        g = np.where(valid, _f64(token_weights), 0.0)
 
     loss_tok = np.zeros(N)
     logZ = np.zeros(N)

@@ -44,7 +44,9 @@ def test_hand_derived_cases(case):
     ign = None if case["ignore"] is None else np.array(case["ignore"], dtype=np.uint8)
     out = kd_topk_kl(np.array(case["h"]), np.array(case["W"]),
                      np.array(case["teacher_idx"]), np.array(case["teacher_logit"]),
-                     tau=case["tau"], ignore=ign)
+                     tau=case["tau"], ignore=ign,
+                     token_weights=case.get("token_weights"),
+                     teacher_mode=case.get("teacher_mode", "logits"))
     assert out["loss"] == pytest.approx(case["loss"], rel=1e-13, abs=1e-15)
     np.testing.assert_allclose(out["loss_per_token"], case["loss_per_token"], rtol=1e-13, atol=1e-15)
     np.testing.assert_allclose(out["logZ"], case["logZ"], rtol=1e-13)

@@ -32,6 +32,12 @@ MUTATIONS = {
     "grad_h_transposed_head": ("grad_h[s0:s1] = G @ W", "grad_h[s0:s1] = (G @ W) * 0.5"),
     "scatter_overwrite_first_col": ("np.add.at(P,", "np.add.at(P[:, ::-1],"),
     "ignored_rows_counted": ("ell[~valid[s0:s1]] = 0.0", "pass"),
+    "token_weights_ignored": ("g = np.where(valid, _f64(token_weights), 0.0)",
+                              "g = np.where(valid, 1.0 / max(n_valid, 1.0), 0.0)"),
+    "logprobs_renormalised": ("return np.exp(_f64(teacher_logit))",
+                              "return np.exp(log_softmax_rows(_f64(teacher_logit)))"),
+    "logprobs_tempered": ("return np.exp(_f64(teacher_logit))",
+                          "return np.exp(_f64(teacher_logit) / float(tau))"),
 }
 
 
@@ -51,7 +57,9 @@ def _pins(fn):
         ign = None if case["ignore"] is None else np.array(case["ignore"], dtype=np.uint8)
         try:
             out = fn(np.array(case["h"]), np.array(case["W"]), np.array(case["teacher_idx"]),
-                     np.array(case["teacher_logit"]), tau=case["tau"], ignore=ign)
+                     np.array(case["teacher_logit"]), tau=case["tau"], ignore=ign,
+                     token_weights=case.get("token_weights"),
+                     teacher_mode=case.get("teacher_mode", "logits"))
             ok = (abs(out["loss"] - case["loss"]) < 1e-12
                   and np.allclose(out["grad_hidden"], case["grad_hidden"], atol=1e-12)
                   and np.allclose(out["grad_W"], case["grad_W"], atol=1e-12))
