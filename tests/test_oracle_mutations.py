@@ -102,6 +102,22 @@ def _pins(fn):
         ok = False
     if not ok:
         failed.append("gibbs")
+    # partial-mass teacher (cached log-probabilities, M < 1) at tau != 1
+    try:
+        lp = np.log(sps.softmax(tl, 1) * 0.6)
+        out = fn(h, W, idx, lp, tau=tau, teacher_mode="logprobs")
+        th = torch.tensor(h, requires_grad=True); tW = torch.tensor(W, requires_grad=True)
+        P = torch.zeros(N, V, dtype=torch.float64)
+        P.scatter_(1, torch.tensor(idx), torch.exp(torch.tensor(lp)))
+        logq = torch.log_softmax(th @ tW.T / tau, 1)
+        per = (P * (torch.where(P > 0, torch.log(P), torch.zeros_like(P)) - logq)).sum(1)
+        per.mean().backward()
+        ok = (abs(out["loss"] - per.mean().item()) < 1e-10
+              and np.allclose(out["grad_W"], tW.grad.numpy(), atol=1e-10))
+    except Exception:
+        ok = False
+    if not ok:
+        failed.append("partial-mass autograd")
     return failed
 
 
