@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KDTOPK_ABI_VERSION 1
+#define KDTOPK_ABI_VERSION 2
 
 typedef enum kd_status {
   KD_OK = 0,
@@ -69,14 +69,28 @@ typedef struct kd_problem {
   int32_t K;           /* cached teacher entries per token; 1 <= K <= V      */
   int32_t dtype;       /* kd_dtype of hidden, W and grad_hidden              */
   float temperature;   /* tau; finite and > 0                                */
-  int32_t flags;       /* reserved; must be 0                                */
+  int32_t flags;       /* 0 or KD_FLAG_TEACHER_LOGPROBS                      */
 } kd_problem;
 
 /*
- * Bytes of device workspace kd_topk_kl_fwd_bwd and kd_topk_kl_check_indices
- * need for problem *p. Pure host function: touches no device. The size is
- * O(N/256 + C_s (V + D + K) + V D): it grows with N only through a per-256-row
- * array of loss partials, never as N*V.
+ * Teacher representation (§3.2). Default (flags = 0): teacher_logit holds
+ * logits of the K cached entries; the teacher distribution is their softmax
+ * over the K entries at temperature tau (retained mass M = 1).
+ * KD_FLAG_TEACHER_LOGPROBS: teacher_logit holds the teacher's log-probabilities
+ * over the full vocabulary at the K cached entries (the partial-mass cache of
+ * §3.2): p = exp(value) as given, M = sum_k p <= 1, no renormalisation and no
+ * temperature (tau still divides the student's logits). Values must be <= 0
+ * and sum_k exp(value) <= 1; this is not checked.
+ */
+#define KD_FLAG_TEACHER_LOGPROBS 1
+
+/*
+ * Bytes of device workspace kd_topk_kl_fwd_bwd, kd_topk_kl_fwd,
+ * kd_topk_kl_bwd and kd_topk_kl_check_indices need for problem *p. Pure host
+ * function: touches no device. The size is O(N/16 + G C_s V + C_s (D + K)),
+ * with G C_s <= 16384 the tokens whose dZ rows one grad_W contraction
+ * gathers: it grows with N only through a per-16-row array of loss partials,
+ * never as N*V.
  * Errors: KD_ERR_NULL_PTR if p or bytes is NULL; the shape/argument errors of
  * kd_topk_kl_fwd_bwd otherwise.
  */
@@ -93,6 +107,8 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  *   teacher_logit [N, K] fp32         teacher logits of the support; the
  *                                     teacher distribution is their softmax
  *                                     over the K entries at temperature tau
+ *                                     (log-probabilities with
+ *                                     KD_FLAG_TEACHER_LOGPROBS)
  *   ignore        [N] uint8 or NULL   nonzero = token excluded from the loss
  *                                     and from the mean's count; NULL = none
  *   loss          [1] fp32            out: mean of l_t over non-ignored
@@ -127,6 +143,69 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p,
                              void* workspace,
                              size_t workspace_bytes,
                              void* hip_stream);
+
+/*
+ * Forward only: the loss of Algorithm 1's two forward passes (normaliser, then
+ * the loss; §3.2.3), without any gradient work, plus the per-token
+ * log-normaliser the backward needs.
+ *
+ *   hidden, W, teacher_idx, teacher_logit, ignore   as for kd_topk_kl_fwd_bwd
+ *   loss          [1] fp32            out: mean of l_t over non-ignored tokens
+ *   loss_per_token [N] fp32 or NULL   out: l_t (0 on ignored tokens)
+ *   saved_logz    [N] fp32            out: log Z_t = logsumexp_v z_tv / tau
+ *   workspace, workspace_bytes, hip_stream   as for kd_topk_kl_fwd_bwd
+ *
+ * Values are bitwise identical to the corresponding outputs of
+ * kd_topk_kl_fwd_bwd. Errors as for kd_topk_kl_fwd_bwd; saved_logz is required.
+ */
+kd_status kd_topk_kl_fwd(const kd_problem* p,
+                         const void* hidden,
+                         const void* W,
+                         const int32_t* teacher_idx,
+                         const float* teacher_logit,
+                         const uint8_t* ignore,
+                         float* loss,
+                         float* loss_per_token,
+                         float* saved_logz,
+                         void* workspace,
+                         size_t workspace_bytes,
+                         void* hip_stream);
+
+/*
+ * Backward only (Algorithm 1's backward: per chunk the logits are recomputed,
+ * q_t = exp(z_t / tau - log Z_t) with log Z_t from the forward, Eq. 3, then
+ * grad_hidden = G W and grad_W (+)= G^T h).
+ *
+ *   hidden, W, teacher_idx, teacher_logit, ignore   as for the forward call
+ *   saved_logz    [N] fp32            log Z_t written by kd_topk_kl_fwd
+ *   grad_loss     [1] fp32 or NULL    upstream gradient of the mean loss
+ *                                     (device scalar); NULL = 1
+ *   grad_loss_per_token [N] fp32 or NULL   upstream gradients u_t of the
+ *                                     per-token losses; when given, G uses
+ *                                     g_t = u_t (ignored tokens 0) instead of
+ *                                     grad_loss / N_valid
+ *   grad_hidden   [N, D] dtype or NULL, grad_W [V, D] fp32 or NULL,
+ *   accumulate_grad_W                 as for kd_topk_kl_fwd_bwd
+ *
+ * With grad_loss = NULL and no per-token gradients the results equal
+ * kd_topk_kl_fwd_bwd's gradients up to the rounding of log Z through fp32.
+ * Errors as for kd_topk_kl_fwd_bwd; saved_logz is required.
+ */
+kd_status kd_topk_kl_bwd(const kd_problem* p,
+                         const void* hidden,
+                         const void* W,
+                         const int32_t* teacher_idx,
+                         const float* teacher_logit,
+                         const uint8_t* ignore,
+                         const float* saved_logz,
+                         const float* grad_loss,
+                         const float* grad_loss_per_token,
+                         void* grad_hidden,
+                         float* grad_W,
+                         int accumulate_grad_W,
+                         void* workspace,
+                         size_t workspace_bytes,
+                         void* hip_stream);
 
 /*
  * Checks that every teacher index lies in [0, V) and that no row repeats an

@@ -16,14 +16,16 @@ LIB_PATH = os.path.join(_HERE, "libkdtopk.so")
 
 KD_F32 = 0
 KD_BF16 = 1
+KD_FLAG_TEACHER_LOGPROBS = 1
 
 STATUS = {
     0: "KD_OK", 1: "KD_ERR_NULL_PTR", 2: "KD_ERR_BAD_SHAPE", 3: "KD_ERR_BAD_ARG",
     4: "KD_ERR_UNSUPPORTED", 5: "KD_ERR_WORKSPACE_TOO_SMALL", 6: "KD_ERR_BAD_INDEX",
     7: "KD_ERR_DEVICE",
 }
-EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_check_indices",
-            "kd_status_string", "kd_abi_version", "kd_profile_enable", "kd_profile_read")
+EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_fwd",
+            "kd_topk_kl_bwd", "kd_topk_kl_check_indices", "kd_status_string", "kd_abi_version",
+            "kd_profile_enable", "kd_profile_read")
 
 
 class KdError(RuntimeError):
@@ -61,6 +63,12 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.kd_topk_kl_fwd_bwd.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp, vp, vp, vp,
                                        vp, ctypes.c_int, vp, sz, vp]
     lib.kd_topk_kl_fwd_bwd.restype = ctypes.c_int
+    lib.kd_topk_kl_fwd.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   sz, vp]
+    lib.kd_topk_kl_fwd.restype = ctypes.c_int
+    lib.kd_topk_kl_bwd.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   vp, ctypes.c_int, vp, sz, vp]
+    lib.kd_topk_kl_bwd.restype = ctypes.c_int
     lib.kd_topk_kl_check_indices.argtypes = [ctypes.POINTER(KdProblem), vp, vp, sz, vp]
     lib.kd_topk_kl_check_indices.restype = ctypes.c_int
     lib.kd_status_string.argtypes = [ctypes.c_int]
@@ -114,26 +122,10 @@ def alloc_workspace(N, D, V, K, chunk, tau, dtype, device):
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
-            chunk: int = 4096, grad_hidden: bool = True, grad_W: bool = True,
-            loss_per_token: bool = False, grad_W_out=None, accumulate_grad_W: bool = False,
-            workspace=None, out=None):
-    """One call of kd_topk_kl_fwd_bwd on the current stream.
-
-    hidden [N, D] and W [V, D] (bf16 or fp32, same dtype), teacher_idx [N, K]
-    int32, teacher_logit [N, K] fp32, ignore [N] uint8 or None. Returns a dict
-    with 'loss' (0-d fp32 tensor), and 'loss_per_token', 'grad_hidden',
-    'grad_W' when requested. `out` may carry preallocated output tensors
-    (keys as returned) to make repeated calls allocation-free.
-    """
+def _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore):
     import torch
-    lib = load_library()
     if hidden.device.type != "cuda":
         raise ValueError("tensors must be on a GPU")
-    N, D = hidden.shape
-    V = W.shape[0]
-    K = teacher_idx.shape[1] if teacher_idx.dim() == 2 else 0
-    dt = _dtype_code(hidden.dtype)
     if W.dtype != hidden.dtype:
         raise TypeError("hidden and W must share a dtype")
     for name, t, want in (("teacher_idx", teacher_idx, torch.int32),
@@ -146,6 +138,27 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
     for t in tensors:
         if not t.is_contiguous():
             raise ValueError("inputs must be contiguous")
+    N, D = hidden.shape
+    K = teacher_idx.shape[1] if teacher_idx.dim() == 2 else 0
+    return N, D, W.shape[0], K, _dtype_code(hidden.dtype)
+
+
+def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
+            chunk: int = 4096, grad_hidden: bool = True, grad_W: bool = True,
+            loss_per_token: bool = False, grad_W_out=None, accumulate_grad_W: bool = False,
+            workspace=None, out=None, teacher_logprobs: bool = False):
+    """One call of kd_topk_kl_fwd_bwd on the current stream.
+
+    hidden [N, D] and W [V, D] (bf16 or fp32, same dtype), teacher_idx [N, K]
+    int32, teacher_logit [N, K] fp32 (log-probabilities of a partial-mass
+    teacher when teacher_logprobs), ignore [N] uint8 or None. Returns a dict
+    with 'loss' (0-d fp32 tensor), and 'loss_per_token', 'grad_hidden',
+    'grad_W' when requested. `out` may carry preallocated output tensors
+    (keys as returned) to make repeated calls allocation-free.
+    """
+    import torch
+    lib = load_library()
+    N, D, V, K, dt = _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore)
     out = dict(out or {})
     dev = hidden.device
     if "loss" not in out:
@@ -159,7 +172,7 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
             out["grad_W"] = grad_W_out
         elif "grad_W" not in out:
             out["grad_W"] = torch.empty(V, D, dtype=torch.float32, device=dev)
-    pr = problem(N, D, V, K, chunk, tau, dt)
+    pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
     rc = lib.kd_topk_kl_fwd_bwd(
@@ -178,6 +191,118 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
     if grad_W:
         res["grad_W"] = out["grad_W"]
     return res
+
+
+def fwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
+        chunk: int = 4096, loss_per_token: bool = False, workspace=None,
+        teacher_logprobs: bool = False):
+    """kd_topk_kl_fwd: the loss without gradient work, plus the per-token
+    log-normaliser log Z the backward needs. Returns a dict with 'loss' (0-d),
+    'saved_logz' [N] and, when requested, 'loss_per_token' [N]."""
+    import torch
+    lib = load_library()
+    N, D, V, K, dt = _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore)
+    dev = hidden.device
+    res = {"loss": torch.empty((), dtype=torch.float32, device=dev),
+           "saved_logz": torch.empty(N, dtype=torch.float32, device=dev)}
+    if loss_per_token:
+        res["loss_per_token"] = torch.empty(N, dtype=torch.float32, device=dev)
+    pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
+    if workspace is None:
+        workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
+    rc = lib.kd_topk_kl_fwd(
+        ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+        _ptr(ignore), _ptr(res["loss"]), _ptr(res.get("loss_per_token")), _ptr(res["saved_logz"]),
+        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
+    if rc != 0:
+        raise KdError(rc, "kd_topk_kl_fwd")
+    return res
+
+
+def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ignore=None,
+        chunk: int = 4096, grad_loss=None, grad_loss_per_token=None, grad_hidden: bool = True,
+        grad_W: bool = True, grad_W_out=None, accumulate_grad_W: bool = False, workspace=None,
+        teacher_logprobs: bool = False):
+    """kd_topk_kl_bwd: gradients from the saved log-normaliser. grad_loss is the
+    upstream gradient of the mean loss (0-d fp32 device tensor, None = 1);
+    grad_loss_per_token [N] fp32 replaces it with per-token upstream gradients.
+    Returns a dict with 'grad_hidden' and 'grad_W' as requested."""
+    import torch
+    lib = load_library()
+    N, D, V, K, dt = _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore)
+    dev = hidden.device
+    for name, t in (("saved_logz", saved_logz), ("grad_loss", grad_loss),
+                    ("grad_loss_per_token", grad_loss_per_token)):
+        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous()):
+            raise TypeError(f"{name} must be a contiguous fp32 tensor")
+    res = {}
+    if grad_hidden:
+        res["grad_hidden"] = torch.empty(N, D, dtype=hidden.dtype, device=dev)
+    if grad_W:
+        res["grad_W"] = grad_W_out if grad_W_out is not None else torch.empty(
+            V, D, dtype=torch.float32, device=dev)
+    pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
+    if workspace is None:
+        workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
+    rc = lib.kd_topk_kl_bwd(
+        ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+        _ptr(ignore), _ptr(saved_logz), _ptr(grad_loss), _ptr(grad_loss_per_token),
+        _ptr(res.get("grad_hidden")), _ptr(res.get("grad_W")), int(bool(accumulate_grad_W)),
+        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
+    if rc != 0:
+        raise KdError(rc, "kd_topk_kl_bwd")
+    return res
+
+
+def _autograd_function():
+    import torch
+
+    class TopKKLLoss(torch.autograd.Function):
+        """Mean top-K KL loss as an autograd function: forward runs
+        kd_topk_kl_fwd and saves log Z; backward runs kd_topk_kl_bwd with the
+        upstream gradient. grad_W is returned in W's dtype (fp32 accumulation
+        inside one call; use bwd(..., accumulate_grad_W=True) to accumulate
+        micro-batches in fp32)."""
+
+        @staticmethod
+        def forward(ctx, hidden, W, teacher_idx, teacher_logit, tau, ignore, chunk,
+                    teacher_logprobs):
+            res = fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore, chunk=chunk,
+                      teacher_logprobs=teacher_logprobs)
+            ctx.save_for_backward(hidden, W, teacher_idx, teacher_logit, res["saved_logz"],
+                                  *([ignore] if ignore is not None else []))
+            ctx.cfg = (tau, chunk, teacher_logprobs, ignore is not None)
+            return res["loss"]
+
+        @staticmethod
+        def backward(ctx, grad_out):
+            tau, chunk, logprobs, has_ignore = ctx.cfg
+            saved = ctx.saved_tensors
+            hidden, W, idx, tl, logz = saved[:5]
+            ignore = saved[5] if has_ignore else None
+            g = grad_out.detach().to(torch.float32).contiguous()
+            need_h, need_W = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
+            res = bwd(hidden, W, idx, tl, logz, tau=tau, ignore=ignore, chunk=chunk, grad_loss=g,
+                      grad_hidden=need_h, grad_W=need_W, teacher_logprobs=logprobs)
+            gW = res.get("grad_W")
+            if gW is not None and gW.dtype != W.dtype:
+                gW = gW.to(W.dtype)
+            return res.get("grad_hidden"), gW, None, None, None, None, None, None
+
+    return TopKKLLoss
+
+
+_TOPK_KL = None
+
+
+def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
+                 chunk: int = 4096, teacher_logprobs: bool = False):
+    """Differentiable mean top-K KL loss (autograd through the split entry points)."""
+    global _TOPK_KL
+    if _TOPK_KL is None:
+        _TOPK_KL = _autograd_function()
+    return _TOPK_KL.apply(hidden, W, teacher_idx, teacher_logit, float(tau), ignore, int(chunk),
+                          bool(teacher_logprobs))
 
 
 def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, workspace=None):

@@ -39,7 +39,7 @@ struct Plan {
 
 kd_status check_problem(const kd_problem* p) {
   if (p == nullptr) return KD_ERR_NULL_PTR;
-  if (p->flags != 0) return KD_ERR_BAD_ARG;
+  if ((p->flags & ~KD_FLAG_TEACHER_LOGPROBS) != 0) return KD_ERR_BAD_ARG;
   if (p->dtype != KD_F32 && p->dtype != KD_BF16) return KD_ERR_UNSUPPORTED;
   if (p->N < 0 || p->N >= kMaxN) return KD_ERR_BAD_SHAPE;
   if (p->D < 64 || p->D > kMaxD) return KD_ERR_BAD_SHAPE;
@@ -140,41 +140,66 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes) {
   return KD_OK;
 }
 
-kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void* W,
-                             const int32_t* teacher_idx, const float* teacher_logit,
-                             const uint8_t* ignore, float* loss, float* loss_per_token,
-                             void* grad_hidden, float* grad_W, int accumulate_grad_W,
-                             void* workspace, size_t workspace_bytes, void* hip_stream) {
-  kd_status st = check_problem(p);
-  if (st != KD_OK) return st;
-  if (loss == nullptr || workspace == nullptr) return KD_ERR_NULL_PTR;
-  if (p->N > 0 && (hidden == nullptr || W == nullptr || teacher_idx == nullptr ||
-                   teacher_logit == nullptr))
-    return KD_ERR_NULL_PTR;
-  if (accumulate_grad_W != 0 && accumulate_grad_W != 1) return KD_ERR_BAD_ARG;
-  if (!aligned16(hidden) || !aligned16(W) || !aligned16(grad_hidden) || !aligned16(grad_W) ||
-      !aligned16(workspace))
-    return KD_ERR_UNSUPPORTED;
-  const Plan pl = make_plan(p);
-  if (workspace_bytes < pl.total) return KD_ERR_WORKSPACE_TOO_SMALL;
+}  // extern "C"
 
-  char* ws = static_cast<char*>(workspace);
+namespace {
+
+// Arguments shared by the three entry points once they are validated.
+struct Call {
+  int mode;
+  const void* hidden;
+  const void* W;
+  const int32_t* idx;
+  const float* tlogit;
+  const uint8_t* ignore;
+  float* loss;              // forward modes
+  float* lpt;
+  float* logz_out;          // forward only
+  const float* logz_in;     // backward only
+  const float* gscale;
+  const float* gtok;
+  void* grad_hidden;        // backward modes
+  float* grad_W;
+  int accumulate;
+  void* ws;
+  size_t ws_bytes;
+  void* stream;
+};
+
+// Common checks: problem, pointers every mode needs, alignment, workspace.
+kd_status validate(const kd_problem* p, const Call& c, const Plan& pl) {
+  if (c.ws == nullptr) return KD_ERR_NULL_PTR;
+  if (p->N > 0 && (c.hidden == nullptr || c.W == nullptr || c.idx == nullptr ||
+                   c.tlogit == nullptr))
+    return KD_ERR_NULL_PTR;
+  if (c.accumulate != 0 && c.accumulate != 1) return KD_ERR_BAD_ARG;
+  if (!aligned16(c.hidden) || !aligned16(c.W) || !aligned16(c.grad_hidden) ||
+      !aligned16(c.grad_W) || !aligned16(c.ws))
+    return KD_ERR_UNSUPPORTED;
+  if (c.ws_bytes < pl.total) return KD_ERR_WORKSPACE_TOO_SMALL;
+  return KD_OK;
+}
+
+// Enqueues Algorithm 1 for one call: the host chunk schedule (§3.2.3).
+kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
+  const bool fwd = c.mode != KD_MODE_BWD, bwd = c.mode != KD_MODE_FWD;
+  char* ws = static_cast<char*>(c.ws);
   int* nvalid = reinterpret_cast<int*>(ws + pl.off_misc);
   float* inv_nvalid = reinterpret_cast<float*>(ws + pl.off_misc + 4);
   float* lossp = reinterpret_cast<float*>(ws + pl.off_lossp);
-  const bool want_dh = grad_hidden != nullptr && pl.N > 0;
-  const bool want_dw = grad_W != nullptr && pl.N > 0;
+  const bool want_dh = bwd && c.grad_hidden != nullptr && pl.N > 0;
+  const bool want_dw = bwd && c.grad_W != nullptr && pl.N > 0;
 
   KdPrepareArgs pa{};
   pa.dtype = p->dtype;
   pa.N = pl.N;
   pa.D = pl.D;
   pa.V = pl.V;
-  pa.ignore = ignore;
+  pa.ignore = c.ignore;
   pa.nvalid = nvalid;
   pa.inv_nvalid = inv_nvalid;
-  pa.zero_gW = (grad_W != nullptr && pl.N == 0 && !accumulate_grad_W) ? grad_W : nullptr;
-  if (kd_launch_prepare(&pa, hip_stream) != 0) return KD_ERR_DEVICE;
+  pa.zero_gW = (bwd && c.grad_W != nullptr && pl.N == 0 && !c.accumulate) ? c.grad_W : nullptr;
+  if (kd_launch_prepare(&pa, c.stream) != 0) return KD_ERR_DEVICE;
 
   float* rows = reinterpret_cast<float*>(ws + pl.off_rows);
   int64_t n_partials = 0;
@@ -185,17 +210,23 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     const int rcount = (int)std::min<int64_t>(pl.c, pl.N - row0);
     KdChunkArgs a{};
     a.dtype = p->dtype;
+    a.mode = c.mode;
+    a.teacher_logprobs = (p->flags & KD_FLAG_TEACHER_LOGPROBS) ? 1 : 0;
+    a.gscale = c.gscale;
+    a.gtok = c.gtok;
+    a.logz_in = c.logz_in;
+    a.logz_out = c.logz_out ? c.logz_out + row0 : nullptr;
     a.D = pl.D;
     a.V = pl.V;
     a.K = (int)pl.K;
     a.row0 = row0;
     a.rows = rcount;
     a.inv_tau = 1.0f / p->temperature;
-    a.W = W;
-    a.Hc = static_cast<const char*>(hidden) + row0 * pl.D * pl.eb;
-    a.tidx = teacher_idx + row0 * pl.K;
-    a.tlogit = teacher_logit;
-    a.ignore = ignore;
+    a.W = c.W;
+    a.Hc = static_cast<const char*>(c.hidden) + row0 * pl.D * pl.eb;
+    a.tidx = c.idx + row0 * pl.K;
+    a.tlogit = c.tlogit;
+    a.ignore = c.ignore;
     a.inv_nvalid = inv_nvalid;
     a.p = reinterpret_cast<float*>(ws + pl.off_p);
     a.rowM = rows;
@@ -215,10 +246,10 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
     a.ldz = pl.Vp;
     a.dh_split = pl.dh_split;
     a.dh_partial = pl.dh_split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
-    a.loss_per_token = loss_per_token ? loss_per_token + row0 : nullptr;
+    a.loss_per_token = c.lpt ? c.lpt + row0 : nullptr;
     a.block_partial = lossp + n_partials;
-    a.gH = want_dh ? static_cast<char*>(grad_hidden) + row0 * pl.D * pl.eb : nullptr;
-    if (kd_launch_chunk(&a, hip_stream) != 0) return KD_ERR_DEVICE;
+    a.gH = want_dh ? static_cast<char*>(c.grad_hidden) + row0 * pl.D * pl.eb : nullptr;
+    if (kd_launch_chunk(&a, c.stream) != 0) return KD_ERR_DEVICE;
     n_partials += cdiv(rcount, 16);
     group_tokens += rcount;
     if (want_dw && (slot == pl.G - 1 || ci == pl.nchunks - 1)) {
@@ -228,18 +259,74 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
       d.V = pl.V;
       d.dZ = ws + pl.off_dz;
       d.ldz = pl.Vp;
-      d.Hg = static_cast<const char*>(hidden) + (row0 + rcount - group_tokens) * pl.D * pl.eb;
+      d.Hg = static_cast<const char*>(c.hidden) + (row0 + rcount - group_tokens) * pl.D * pl.eb;
       d.tokens = group_tokens;
-      d.beta = (dw_done || accumulate_grad_W) ? 1 : 0;
-      d.gW = grad_W;
-      if (kd_launch_dw(&d, hip_stream) != 0) return KD_ERR_DEVICE;
+      d.beta = (dw_done || c.accumulate) ? 1 : 0;
+      d.gW = c.grad_W;
+      if (kd_launch_dw(&d, c.stream) != 0) return KD_ERR_DEVICE;
       dw_done = true;
       group_tokens = 0;
     }
   }
-  if (kd_launch_finalize(lossp, (int)n_partials, inv_nvalid, loss, hip_stream) != 0)
+  if (fwd && kd_launch_finalize(lossp, (int)n_partials, inv_nvalid, c.loss, c.stream) != 0)
     return KD_ERR_DEVICE;
   return KD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void* W,
+                             const int32_t* teacher_idx, const float* teacher_logit,
+                             const uint8_t* ignore, float* loss, float* loss_per_token,
+                             void* grad_hidden, float* grad_W, int accumulate_grad_W,
+                             void* workspace, size_t workspace_bytes, void* hip_stream) {
+  kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  if (loss == nullptr) return KD_ERR_NULL_PTR;
+  const Call c{KD_MODE_FWD_BWD, hidden, W, teacher_idx, teacher_logit, ignore, loss,
+               loss_per_token, nullptr, nullptr, nullptr, nullptr, grad_hidden, grad_W,
+               accumulate_grad_W, workspace, workspace_bytes, hip_stream};
+  const Plan pl = make_plan(p);
+  st = validate(p, c, pl);
+  if (st != KD_OK) return st;
+  return enqueue(p, pl, c);
+}
+
+kd_status kd_topk_kl_fwd(const kd_problem* p, const void* hidden, const void* W,
+                         const int32_t* teacher_idx, const float* teacher_logit,
+                         const uint8_t* ignore, float* loss, float* loss_per_token,
+                         float* saved_logz, void* workspace, size_t workspace_bytes,
+                         void* hip_stream) {
+  kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  if (loss == nullptr || (p->N > 0 && saved_logz == nullptr)) return KD_ERR_NULL_PTR;
+  const Call c{KD_MODE_FWD, hidden, W, teacher_idx, teacher_logit, ignore, loss,
+               loss_per_token, saved_logz, nullptr, nullptr, nullptr, nullptr, nullptr, 0,
+               workspace, workspace_bytes, hip_stream};
+  const Plan pl = make_plan(p);
+  st = validate(p, c, pl);
+  if (st != KD_OK) return st;
+  return enqueue(p, pl, c);
+}
+
+kd_status kd_topk_kl_bwd(const kd_problem* p, const void* hidden, const void* W,
+                         const int32_t* teacher_idx, const float* teacher_logit,
+                         const uint8_t* ignore, const float* saved_logz,
+                         const float* grad_loss, const float* grad_loss_per_token,
+                         void* grad_hidden, float* grad_W, int accumulate_grad_W,
+                         void* workspace, size_t workspace_bytes, void* hip_stream) {
+  kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  if (p->N > 0 && saved_logz == nullptr) return KD_ERR_NULL_PTR;
+  const Call c{KD_MODE_BWD, hidden, W, teacher_idx, teacher_logit, ignore, nullptr, nullptr,
+               nullptr, saved_logz, grad_loss, grad_loss_per_token, grad_hidden, grad_W,
+               accumulate_grad_W, workspace, workspace_bytes, hip_stream};
+  const Plan pl = make_plan(p);
+  st = validate(p, c, pl);
+  if (st != KD_OK) return st;
+  return enqueue(p, pl, c);
 }
 
 kd_status kd_topk_kl_check_indices(const kd_problem* p, const int32_t* teacher_idx,

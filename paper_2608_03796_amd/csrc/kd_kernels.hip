@@ -42,27 +42,37 @@ __global__ void k_fill_f32(float* p, int64_t n, float v) {
 }
 
 // Teacher distribution over the K cached entries of each chunk row (§3.2):
-// p = softmax(teacher_logit / tau), M = sum p, H = sum p log p (0 log 0 = 0),
-// coef = g/tau with g = 1/N_valid (0 for ignored rows). One wave per row.
+// p = softmax(teacher_logit / tau), or p = exp(value) as given for cached
+// log-probabilities (partial mass); M = sum p, H = sum p log p (0 log 0 = 0).
+// Row weight coef = g/tau, g = 1/N_valid times the upstream gradient of the
+// mean (gscale, default 1), or the upstream gradient of the token's own loss
+// (gtok); 0 for ignored rows. With a saved log-normaliser (backward only) the
+// row's log2 Z is set from it. One wave per row.
 __global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, int64_t row0,
-                                   int rows, int K, float inv_tau, const float* inv_nvalid,
-                                   float* p_out, float* rowM, float* rowH, float* rowCoef,
-                                   float* rowCoefM) {
+                                   int rows, int K, float inv_tau, int logprobs,
+                                   const float* inv_nvalid, const float* gscale,
+                                   const float* gtok, const float* logz_in, float* p_out,
+                                   float* rowM, float* rowH, float* rowCoef, float* rowCoefM,
+                                   float* rowL2) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
   const int64_t t = row0 + r;
   const float* u = tlogit + t * (int64_t)K;
-  float mx = -INFINITY;
-  for (int k = lane; k < K; k += 64) mx = fmaxf(mx, u[k] * inv_tau);
-  mx = wave_max(mx);
-  float s = 0.f;
-  for (int k = lane; k < K; k += 64) s += expf(u[k] * inv_tau - mx);
-  s = wave_sum(s);
-  const float logs = logf(s);
+  float mx = 0.f, logs = 0.f, scale = 1.f;
+  if (!logprobs) {
+    mx = -INFINITY;
+    for (int k = lane; k < K; k += 64) mx = fmaxf(mx, u[k] * inv_tau);
+    mx = wave_max(mx);
+    float s = 0.f;
+    for (int k = lane; k < K; k += 64) s += expf(u[k] * inv_tau - mx);
+    s = wave_sum(s);
+    logs = logf(s);
+    scale = inv_tau;
+  }
   float m = 0.f, h = 0.f;
   for (int k = lane; k < K; k += 64) {
-    const float lp = u[k] * inv_tau - mx - logs;
+    const float lp = u[k] * scale - mx - logs;
     const float pk = expf(lp);
     p_out[(int64_t)r * K + k] = pk;
     m += pk;
@@ -72,11 +82,13 @@ __global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, i
   h = wave_sum(h);
   if (lane == 0) {
     const bool valid = ignore == nullptr || ignore[t] == 0;
-    const float coef = valid ? inv_tau * inv_nvalid[0] : 0.f;
+    const float g = gtok != nullptr ? gtok[t] : inv_nvalid[0] * (gscale != nullptr ? gscale[0] : 1.f);
+    const float coef = valid ? inv_tau * g : 0.f;
     rowM[r] = m;
     rowH[r] = h;
     rowCoef[r] = coef;
     rowCoefM[r] = coef * m;
+    if (logz_in != nullptr) rowL2[r] = logz_in[t] * kLog2e;
   }
 }
 
@@ -424,8 +436,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
 // deterministic mean.
 constexpr int kLossRows = 16;  // rows per row-loss block (4 per wave)
 __global__ void k_row_loss(const float* zhit, const float* p, int K, const float* rowL2,
-                           const float* rowM, const float* rowH, const float* rowCoef, int rows,
-                           float inv_tau, float* loss_per_token, float* block_partial) {
+                           const float* rowM, const float* rowH, const uint8_t* ignore,
+                           int64_t row0, int rows, float inv_tau, float* loss_per_token,
+                           float* logz_out, float* block_partial) {
   // one fixed-order partial per block
   __shared__ float red[4];
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -443,9 +456,11 @@ __global__ void k_row_loss(const float* zhit, const float* p, int K, const float
     const int r = blockIdx.x * kLossRows + wave * 4 + rr;
     const float cs = wave_sum(c[rr]);
     if (r >= rows) continue;
-    const float l = rowCoef[r] != 0.f ? rowH[r] - cs * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
+    const bool valid = ignore == nullptr || ignore[row0 + r] == 0;
+    const float l = valid ? rowH[r] - cs * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
     if (lane == 0) {
       if (loss_per_token) loss_per_token[r] = l;
+      if (logz_out) logz_out[r] = rowL2[r] * kLn2;
       acc += l;
     }
   }
@@ -732,40 +747,44 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
   const float k2 = kLog2e * a.inv_tau;
   const double gemm_flops = 2.0 * (double)a.rows * (double)a.D * (double)a.V;
 
+  const bool fwd = a.mode != KD_MODE_BWD, bwd = a.mode != KD_MODE_FWD;
 {
     ProfScope ps_(P_PROLOGUE, 0.0, s);
     hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
-                     a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.inv_nvalid, a.p, a.rowM, a.rowH,
-                     a.rowCoef, a.rowCoefM);
+                     a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.teacher_logprobs, a.inv_nvalid,
+                     a.gscale, a.gtok, fwd ? nullptr : a.logz_in, a.p, a.rowM, a.rowH, a.rowCoef,
+                     a.rowCoefM, a.rowL2);
     }
 {
     ProfScope ps_(P_BUCKET, 0.0, s);
     hipLaunchKernelGGL(k_bucket, dim3(TNt), dim3(kBucketThreads), 0, s, a.tidx, a.p, a.rows, a.K,
                        (int)a.V, a.nVT, a.hits, a.hitp, a.hoff, a.zhit);
     }
-{
-    ProfScope ps_(P_LOGITS, gemm_flops, s);
-    hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
-                     (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT);
+  if (fwd) {
+    {
+      ProfScope ps_(P_LOGITS, gemm_flops, s);
+      hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
+                         (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT);
     }
-{
-    ProfScope ps_(P_MERGE, 0.0, s);
-    hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
-                     a.rows, a.nVT, a.rowL2);
+    {
+      ProfScope ps_(P_MERGE, 0.0, s);
+      hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
+                         a.rows, a.nVT, a.rowL2);
     }
+  }
 {
     ProfScope ps_(P_DZ, gemm_flops, s);
     hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
                      a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits, a.hitp, a.hoff,
                      a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz, a.zhit);
     }
-{
+  if (fwd) {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
-    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(256), 0, s, a.zhit, a.p, a.K,
-                     a.rowL2, a.rowM, a.rowH, a.rowCoef, a.rows, a.inv_tau, a.loss_per_token,
-                     a.block_partial);
-    }
-  if (a.gH != nullptr) {
+    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(256), 0, s, a.zhit, a.p,
+                       a.K, a.rowL2, a.rowM, a.rowH, a.ignore, a.row0, a.rows, a.inv_tau,
+                       a.loss_per_token, a.logz_out, a.block_partial);
+  }
+  if (bwd && a.gH != nullptr) {
     const int TM = cdiv(a.rows, kTile), TN = cdiv(a.D, kTile);
     const int ks = (int)(a.ldz * sizeof(T) / kRowB);
 {

@@ -14,8 +14,16 @@ struct KdPrepareArgs {
   float* zero_gW;           // grad_W to clear, or null
 };
 
+enum { KD_MODE_FWD_BWD = 0, KD_MODE_FWD = 1, KD_MODE_BWD = 2 };
+
 struct KdChunkArgs {
   int dtype;
+  int mode;                 // KD_MODE_*: which half of Algorithm 1 runs
+  int teacher_logprobs;     // cached log-probabilities (partial mass) instead of logits
+  const float* gscale;      // upstream gradient of the mean (device scalar) or null = 1
+  const float* gtok;        // full [N] upstream per-token gradients or null
+  const float* logz_in;     // full [N] saved log Z (backward only) or null
+  float* logz_out;          // this chunk's rows of the saved log Z (forward) or null
   int64_t D, V;
   int K;
   int64_t row0;             // first token of the chunk

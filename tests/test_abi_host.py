@@ -63,11 +63,17 @@ def _ws(lib, pr):
     (dict(D=96), 4), (dict(V=0), 2), (dict(V=2 ** 20 + 1), 2), (dict(K=0), 2),
     (dict(K=4097), 2), (dict(chunk=0), 3), (dict(chunk=-5), 3), (dict(tau=0.0), 3),
     (dict(tau=-1.0), 3), (dict(tau=float("inf")), 3), (dict(tau=float("nan")), 3),
-    (dict(dtype=2), 4), (dict(dtype=-1), 4), (dict(flags=1), 3),
+    (dict(dtype=2), 4), (dict(dtype=-1), 4), (dict(flags=2), 3), (dict(flags=-1), 3),
 ])
 def test_workspace_size_rejects(lib, kw, code):
     rc, _ = _ws(lib, _prob(**kw))
     assert rc == code
+
+
+def test_teacher_logprobs_flag_accepted(lib):
+    rc, b = _ws(lib, _prob(flags=kd.KD_FLAG_TEACHER_LOGPROBS))
+    rc0, b0 = _ws(lib, _prob())
+    assert rc == rc0 == 0 and b == b0
 
 
 def test_workspace_size_null(lib):
@@ -154,3 +160,69 @@ def test_check_indices_rejects(lib):
                                         ctypes.c_size_t(1 << 40), None) == 1
     assert lib.kd_topk_kl_check_indices(ctypes.byref(pr), ctypes.c_void_p(FAKE),
                                         ctypes.c_void_p(FAKE), ctypes.c_size_t(16), None) == 5
+
+
+# ------------------------------------------------ split forward / backward --
+def _fwd(lib, pr, hidden=FAKE, W=FAKE, idx=FAKE, logit=FAKE, ignore=None, loss=FAKE, lpt=None,
+         logz=FAKE, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        rc, ws_bytes = _ws(lib, pr)
+        if rc != 0:
+            ws_bytes = 1 << 40
+    v = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.kd_topk_kl_fwd(ctypes.byref(pr), v(hidden), v(W), v(idx), v(logit), v(ignore),
+                              v(loss), v(lpt), v(logz), v(ws), ctypes.c_size_t(ws_bytes), None)
+
+
+def _bwd(lib, pr, hidden=FAKE, W=FAKE, idx=FAKE, logit=FAKE, ignore=None, logz=FAKE, gl=None,
+         glt=None, gh=FAKE, gw=FAKE, acc=0, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        rc, ws_bytes = _ws(lib, pr)
+        if rc != 0:
+            ws_bytes = 1 << 40
+    v = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.kd_topk_kl_bwd(ctypes.byref(pr), v(hidden), v(W), v(idx), v(logit), v(ignore),
+                              v(logz), v(gl), v(glt), v(gh), v(gw), acc, v(ws),
+                              ctypes.c_size_t(ws_bytes), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(N=-3), 2), (dict(D=100), 4), (dict(K=5000), 2), (dict(chunk=0), 3),
+    (dict(tau=0.0), 3), (dict(dtype=7), 4), (dict(flags=2), 3),
+])
+def test_split_rejects_problem(lib, kw, code):
+    assert _fwd(lib, _prob(**kw)) == code
+    assert _bwd(lib, _prob(**kw)) == code
+
+
+@pytest.mark.parametrize("field", ["hidden", "W", "idx", "logit", "loss", "logz", "ws"])
+def test_fwd_null_pointers(lib, field):
+    assert _fwd(lib, _prob(), **{field: None}) == 1
+
+
+@pytest.mark.parametrize("field", ["hidden", "W", "idx", "logit", "logz", "ws"])
+def test_bwd_null_pointers(lib, field):
+    assert _bwd(lib, _prob(), **{field: None}) == 1
+
+
+@pytest.mark.parametrize("field", ["hidden", "W", "ws"])
+def test_fwd_misaligned(lib, field):
+    assert _fwd(lib, _prob(), **{field: FAKE_MISALIGNED}) == 4
+
+
+@pytest.mark.parametrize("field", ["hidden", "W", "gh", "gw", "ws"])
+def test_bwd_misaligned(lib, field):
+    assert _bwd(lib, _prob(), **{field: FAKE_MISALIGNED}) == 4
+
+
+def test_split_workspace_too_small(lib):
+    pr = _prob()
+    rc, need = _ws(lib, pr)
+    assert rc == 0
+    assert _fwd(lib, pr, ws_bytes=need - 1) == 5
+    assert _bwd(lib, pr, ws_bytes=need - 1) == 5
+
+
+@pytest.mark.parametrize("acc", [2, -1])
+def test_bwd_bad_accumulate(lib, acc):
+    assert _bwd(lib, _prob(), acc=acc) == 3

@@ -1,0 +1,175 @@
+"""GPU parity of the split forward/backward entry points (Algorithm 1's own
+structure), the upstream gradients they take, the autograd wrapper built on
+them, and the partial-mass teacher mode, all against the fp64 oracle on the
+same seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+import kd_inputs as ki
+from oracle import kd_topk_kl
+from tests.helpers import TOL, oracle_inputs, rel_max, to64
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # N, D, V, K, chunk, tau, ignore fraction
+    (259, 128, 4133, 7, 100, 2.0, 0.2),
+    (513, 192, 1000, 16, 513, 1.0, 0.0),
+]
+
+
+def _inputs(N, D, V, K, dtype, seed=0, ignore_frac=0.0):
+    dev = "cuda"
+    hidden = ki.make_hidden(N, D, dtype, dev, seed=ki.SEED_HIDDEN + seed)
+    W = ki.make_weight(V, D, dtype, dev, seed=ki.SEED_W + seed)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + seed)
+    ignore = None
+    if ignore_frac > 0:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(ki.SEED_MASK + seed)
+        ignore = (torch.rand(N, generator=g) < ignore_frac).to(torch.uint8).to(dev)
+    return dict(hidden=hidden, W=W, teacher_idx=idx, teacher_logit=logit, ignore=ignore)
+
+
+def _logprob_teacher(inp, seed):
+    """Partial-mass cache: the K entries keep a per-row mass in [0.3, 0.95]."""
+    tl = inp["teacher_logit"]
+    g = torch.Generator(device="cpu")
+    g.manual_seed(ki.SEED_TEACHER + 100 + seed)
+    mass = (0.3 + 0.65 * torch.rand(tl.shape[0], generator=g)).to(tl.device)
+    return (torch.log_softmax(tl, dim=1) + torch.log(mass)[:, None]).contiguous()
+
+
+def _args(inp):
+    return (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,D,V,K,chunk,tau,ign", SHAPES)
+def test_forward_matches_fused_and_oracle(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
+    kd = gpu_lib
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=N + 1, ignore_frac=ign)
+    f = kd.fwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True)
+    fb = kd.fwd_bwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True,
+                    grad_hidden=False, grad_W=False)
+    torch.cuda.synchronize()
+    # the same kernels compute the loss in both entry points
+    assert torch.equal(f["loss"], fb["loss"])
+    assert torch.equal(f["loss_per_token"], fb["loss_per_token"])
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk, want_grads=False)
+    tol = TOL[dtype]
+    assert abs(float(f["loss"]) - ref["loss"]) <= tol["loss"] * abs(ref["loss"])
+    # log Z from fp32 accumulation of the same inputs: absolute error ~1e-6 |log Z|
+    assert np.abs(to64(f["saved_logz"]) - ref["logZ"]).max() <= 1e-5 * np.abs(ref["logZ"]).max()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,D,V,K,chunk,tau,ign", SHAPES)
+def test_backward_matches_oracle(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
+    kd = gpu_lib
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=N + 2, ignore_frac=ign)
+    f = kd.fwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk)
+    b = kd.bwd(*_args(inp), f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk)
+    torch.cuda.synchronize()
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk)
+    tol = TOL[dtype]
+    assert rel_max(to64(b["grad_hidden"]), ref["grad_hidden"]) <= tol["grad"]
+    assert rel_max(to64(b["grad_W"]), ref["grad_W"]) <= tol["grad"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_upstream_scalar_and_per_token(gpu_lib, dtype):
+    kd = gpu_lib
+    N, D, V, K, chunk, tau = 259, 128, 4133, 7, 100, 2.0
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=3, ignore_frac=0.2)
+    f = kd.fwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk)
+    tol = TOL[dtype]
+    o = oracle_inputs(inp)
+    valid = (o["ignore"] == 0)
+    # scalar upstream gradient of the mean
+    gl = torch.tensor(-2.5, dtype=torch.float32, device="cuda")
+    b = kd.bwd(*_args(inp), f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk, grad_loss=gl)
+    ref = kd_topk_kl(**o, tau=tau, chunk=chunk,
+                     token_weights=np.full(N, -2.5 / valid.sum()))
+    assert rel_max(to64(b["grad_hidden"]), ref["grad_hidden"]) <= tol["grad"]
+    assert rel_max(to64(b["grad_W"]), ref["grad_W"]) <= tol["grad"]
+    # per-token upstream gradients (ignored rows get none)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(4242)
+    u = (torch.rand(N, generator=g) * 3.0 - 1.0).to("cuda")
+    b = kd.bwd(*_args(inp), f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk,
+               grad_loss_per_token=u)
+    torch.cuda.synchronize()
+    ref = kd_topk_kl(**o, tau=tau, chunk=chunk, token_weights=to64(u))
+    assert rel_max(to64(b["grad_hidden"]), ref["grad_hidden"]) <= tol["grad"]
+    assert rel_max(to64(b["grad_W"]), ref["grad_W"]) <= tol["grad"]
+    assert torch.all(b["grad_hidden"][inp["ignore"].bool()] == 0)
+
+
+def test_backward_accumulates_grad_W(gpu_lib):
+    kd = gpu_lib
+    inp = _inputs(300, 64, 777, 5, torch.float32, seed=9)
+    f = kd.fwd(*_args(inp), tau=1.0, chunk=64)
+    one = kd.bwd(*_args(inp), f["saved_logz"], tau=1.0, chunk=64, grad_hidden=False)["grad_W"]
+    acc = one.clone()
+    kd.bwd(*_args(inp), f["saved_logz"], tau=1.0, chunk=64, grad_hidden=False, grad_W_out=acc,
+           accumulate_grad_W=True)
+    torch.cuda.synchronize()
+    assert torch.allclose(acc, 2 * one, rtol=1e-6, atol=1e-12)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_autograd_wrapper(gpu_lib, dtype):
+    kd = gpu_lib
+    N, D, V, K, chunk, tau = 259, 128, 4133, 7, 100, 2.0
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=11, ignore_frac=0.2)
+    h = inp["hidden"].clone().requires_grad_(True)
+    W = inp["W"].clone().requires_grad_(True)
+    loss = kd.topk_kl_loss(h, W, inp["teacher_idx"], inp["teacher_logit"], tau=tau,
+                           ignore=inp["ignore"], chunk=chunk)
+    (3.0 * loss).backward()
+    torch.cuda.synchronize()
+    o = oracle_inputs(inp)
+    valid = (o["ignore"] == 0)
+    ref = kd_topk_kl(**o, tau=tau, chunk=chunk, token_weights=np.full(N, 3.0 / valid.sum()))
+    tol = TOL[dtype]
+    assert abs(float(loss) - ref["loss"]) <= tol["loss"] * abs(ref["loss"])
+    assert h.grad.dtype == tdt and W.grad.dtype == tdt
+    assert rel_max(to64(h.grad), ref["grad_hidden"]) <= tol["grad"]
+    # grad_W comes back in W's dtype: bf16 rounding of an fp32 result
+    assert rel_max(to64(W.grad), ref["grad_W"]) <= tol["grad"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("tau", [1.0, 2.0])
+def test_partial_mass_teacher(gpu_lib, dtype, tau):
+    """Cached log-probabilities (retained mass M < 1, §3.2): fused and split
+    entry points against the oracle's partial-mass mode."""
+    kd = gpu_lib
+    N, D, V, K, chunk = 259, 128, 4133, 7, 100
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=17, ignore_frac=0.1)
+    inp["teacher_logit"] = _logprob_teacher(inp, 17)
+    tol = TOL[dtype]
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk, teacher_mode="logprobs")
+    fb = kd.fwd_bwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True,
+                    teacher_logprobs=True)
+    f = kd.fwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, teacher_logprobs=True)
+    b = kd.bwd(*_args(inp), f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk,
+               teacher_logprobs=True)
+    torch.cuda.synchronize()
+    for loss in (fb["loss"], f["loss"]):
+        assert abs(float(loss) - ref["loss"]) <= tol["loss"] * abs(ref["loss"])
+    assert rel_max(to64(fb["loss_per_token"]), ref["loss_per_token"]) <= tol["loss"]
+    for res in (fb, b):
+        assert rel_max(to64(res["grad_hidden"]), ref["grad_hidden"]) <= tol["grad"]
+        assert rel_max(to64(res["grad_W"]), ref["grad_W"]) <= tol["grad"]
+    # Gibbs bound of the partial-mass loss, per token: l >= M log M
+    M = ref["M"]
+    lpt = to64(fb["loss_per_token"])
+    valid = to64(inp["ignore"]) == 0
+    assert np.all(lpt[valid] >= (M * np.log(M))[valid] - 1e-4)
