@@ -155,8 +155,10 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p,
  *   saved_logz    [N] fp32            out: log Z_t = logsumexp_v z_tv / tau
  *   workspace, workspace_bytes, hip_stream   as for kd_topk_kl_fwd_bwd
  *
- * Values are bitwise identical to the corresponding outputs of
- * kd_topk_kl_fwd_bwd. Errors as for kd_topk_kl_fwd_bwd; saved_logz is required.
+ * One projection per chunk (the normaliser and the student logits at the
+ * teacher entries come from the same tile). Values are bitwise identical to
+ * the corresponding outputs of kd_topk_kl_fwd_bwd. Errors as for
+ * kd_topk_kl_fwd_bwd; saved_logz is required.
  */
 kd_status kd_topk_kl_fwd(const kd_problem* p,
                          const void* hidden,

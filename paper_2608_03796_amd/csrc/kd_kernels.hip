@@ -98,12 +98,31 @@ __global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, i
 // y = z log2(e)/tau are reduced in registers, across the four lane groups of
 // the wave, and across the two waves sharing the tokens through LDS. Output per (token,
 // vocabulary tile): (max, sum) in base-2 units.
+//
+// With zhit set (forward-only calls, which have no logit recompute), the tile
+// also records z at its teacher entries for C = sum_k p z (Eq. 2), in O(1)
+// per entry: the entries of the tile's bucket mark a 256 x 256 bit map of
+// cells (token, column) in LDS; an exclusive prefix sum of the words' bit
+// counts numbers the marked cells; the lane holding a marked cell stores its
+// z at that number in an LDS array; then every entry reads the z of its cell.
+// A tile with more marked cells than the array holds (a teacher whose
+// entries crowd one vocabulary tile) has the holders of the excess cells
+// search the bucket for their entries instead.
+constexpr int kZhBits = 0;                      // LDS: 256 tokens x 8 words
+constexpr int kZhPre = 8192;                    // exclusive prefix per word
+constexpr int kZhWs = 16384;                    // per-wave totals of the scan
+constexpr int kZhVal = 16384 + 64;              // z of the marked cells
+constexpr int kZhCap = (kLdsMain - kZhVal) / 4; // 28656 cells
+
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict__ W,
                                                             const T* __restrict__ Hc, int D,
                                                             int V, int rows, int TM, int TN,
                                                             float k2, float* part_m,
-                                                            float* part_s, int nVT) {
+                                                            float* part_s, int nVT,
+                                                            const uint32_t* __restrict__ hits,
+                                                            const int* __restrict__ hoff, int K,
+                                                            float* zhit) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
@@ -119,6 +138,76 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
   const bool full = m0 + kTile <= V;
+  if (zhit != nullptr) {
+    const int tid = threadIdx.x;
+    const int64_t seg = (int64_t)nt * kTile * K;
+    const int* ho = hoff + (int64_t)nt * (nVT + 1) + mt;
+    const int hb = ho[0], cnt = ho[1] - hb;
+    const uint32_t* hl = hits + seg + hb;
+    uint32_t* bits = reinterpret_cast<uint32_t*>(lds + kZhBits);
+    int* pre = reinterpret_cast<int*>(lds + kZhPre);
+    int* wsum = reinterpret_cast<int*>(lds + kZhWs);
+    float* zval = reinterpret_cast<float*>(lds + kZhVal);
+    *reinterpret_cast<u32x4_t*>(bits + 4 * tid) = u32x4_t{0u, 0u, 0u, 0u};
+    __syncthreads();
+    for (int q = tid; q < cnt; q += kThreads) {
+      const uint32_t e = hl[q];
+      const int tl = (int)(e & 255u), vl = (int)((e >> 8) & 255u);
+      atomicOr(&bits[tl * 8 + (vl >> 5)], 1u << (vl & 31));
+    }
+    __syncthreads();
+    // exclusive prefix of the 2048 word counts: thread tid owns words 4 tid .. 4 tid + 3
+    {
+      const u32x4_t wd = *reinterpret_cast<const u32x4_t*>(bits + 4 * tid);
+      const int c0 = __builtin_popcount(wd[0]), c1 = __builtin_popcount(wd[1]);
+      const int c2 = __builtin_popcount(wd[2]), c3 = __builtin_popcount(wd[3]);
+      const int run = c0 + c1 + c2 + c3;
+      const int incl = wave_incl_scan(run);
+      if (lane == 63) wsum[wave] = incl;
+      __syncthreads();
+      int base = incl - run;
+      for (int w = 0; w < wave; ++w) base += wsum[w];
+      *reinterpret_cast<i32x4_t*>(pre + 4 * tid) =
+          i32x4_t{base, base + c0, base + c0 + c1, base + c0 + c1 + c2};
+    }
+    __syncthreads();
+    const int g = lane >> 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = acc_n(wn, j, lane);  // token in the tile
+      const u32x4_t wd = *reinterpret_cast<const u32x4_t*>(bits + n * 8 + wm * 4);
+      const i32x4_t wp = *reinterpret_cast<const i32x4_t*>(pre + n * 8 + wm * 4);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int sh = 16 * (i & 1) + 4 * g;  // bit of the cell's first column in its word
+        const uint32_t nib = (wd[i >> 1] >> sh) & 15u;
+        if (nib == 0u) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (((nib >> r) & 1u) == 0u) continue;
+          const int rank = wp[i >> 1] + __builtin_popcount(wd[i >> 1] & ((1u << (sh + r)) - 1u));
+          if (rank < kZhCap) {
+            zval[rank] = acc.v[i][j][r];
+          } else {
+            const uint32_t cell = (uint32_t)n | ((uint32_t)acc_m(wm, i, lane, r) << 8);
+            for (int q = 0; q < cnt; ++q) {
+              const uint32_t e = hl[q];
+              if ((e & 0xffffu) == cell) zhit[(int64_t)(n0 + n) * K + (e >> 16)] = acc.v[i][j][r];
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int q = tid; q < cnt; q += kThreads) {
+      const uint32_t e = hl[q];
+      const int tl = (int)(e & 255u), vl = (int)((e >> 8) & 255u);
+      const int w = tl * 8 + (vl >> 5);
+      const int rank = pre[w] + __builtin_popcount(bits[w] & ((1u << (vl & 31)) - 1u));
+      if (rank < kZhCap) zhit[(int64_t)(n0 + tl) * K + (e >> 16)] = zval[rank];
+    }
+    __syncthreads();
+  }
   float* xch = reinterpret_cast<float*>(lds);  // [wn][j][16 lanes][max, sum]
   float rm[4], rs[4];
 #pragma unroll
@@ -394,7 +483,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
       const int n = tl & 127, v = (int)((e >> 8) & 255u), k = (int)(e >> 16);
       float* cell = st + n * 256 + ((((v >> 2) ^ hsw16(n)) << 2) | (v & 3));
       const float z = *cell;
-      zhit[(int64_t)(n0 + tl) * K + k] = z;
+      if (zhit != nullptr) zhit[(int64_t)(n0 + tl) * K + k] = z;
       *cell = rs_cm[tl] * fast_exp2(z * k2 - rs_l2[tl]) - rs_cf[tl] * pk;
       atomicOr(&hbits[n * 8 + (v >> 5)], 1u << (v & 31));
     };
@@ -763,8 +852,11 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
   if (fwd) {
     {
       ProfScope ps_(P_LOGITS, gemm_flops, s);
+      // forward-only: z at the teacher entries comes from this GEMM, and
+      // there is no logit recompute
       hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
-                         (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT);
+                         (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT, a.hits,
+                         a.hoff, a.K, bwd ? nullptr : a.zhit);
     }
     {
       ProfScope ps_(P_MERGE, 0.0, s);
@@ -772,12 +864,14 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                          a.rows, a.nVT, a.rowL2);
     }
   }
-{
+  if (bwd) {
+    // z at the teacher entries is recorded here in the fused call (the
+    // backward-only call has no use for it)
     ProfScope ps_(P_DZ, gemm_flops, s);
     hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
-                     a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits, a.hitp, a.hoff,
-                     a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz, a.zhit);
-    }
+                       a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits, a.hitp,
+                       a.hoff, a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz, fwd ? a.zhit : nullptr);
+  }
   if (fwd) {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
     hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(256), 0, s, a.zhit, a.p,

@@ -173,3 +173,28 @@ def test_partial_mass_teacher(gpu_lib, dtype, tau):
     lpt = to64(fb["loss_per_token"])
     valid = to64(inp["ignore"]) == 0
     assert np.all(lpt[valid] >= (M * np.log(M))[valid] - 1e-4)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_teacher_crowding_one_vocab_tile(gpu_lib, dtype):
+    """Every token's K = 128 entries lie in the same 256-column vocabulary tile,
+    so the first 256-token tile has 32768 teacher cells in one output tile: more than
+    the forward-only kernel numbers in LDS (28656), so some cells take the
+    bucket-search path. The loss must match the fused entry point bit for bit
+    and the oracle within tolerance."""
+    kd = gpu_lib
+    N, D, V, K, chunk, tau = 300, 64, 1100, 128, 300, 1.5
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=21)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(ki.SEED_TEACHER + 21)
+    tile = torch.full((N,), 2)   # columns [512, 768), a full tile
+    perm = torch.argsort(torch.rand(N, 256, generator=g), dim=1)[:, :K]
+    inp["teacher_idx"] = (tile[:, None] * 256 + perm).to(torch.int32).to("cuda").contiguous()
+    f = kd.fwd(*_args(inp), tau=tau, chunk=chunk, loss_per_token=True)
+    fb = kd.fwd_bwd(*_args(inp), tau=tau, chunk=chunk, loss_per_token=True, grad_hidden=False,
+                    grad_W=False)
+    torch.cuda.synchronize()
+    assert torch.equal(f["loss_per_token"], fb["loss_per_token"])
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk, want_grads=False)
+    assert abs(float(f["loss"]) - ref["loss"]) <= TOL[dtype]["loss"] * abs(ref["loss"])
