@@ -452,7 +452,6 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   const float* hp = reinterpret_cast<const float*>(lds + kDzHits + 4 * kDzHitCap);
   uint32_t* hbits = reinterpret_cast<uint32_t*>(lds + kDzBits);
   const int vl0 = 4 * lane;  // this lane's 4 vocabulary columns in the row pass
-  const bool vfull = m0 + kTile <= V;
 
   // unrolled: a loop header here would make the compiler wait for the first
   // half's dZ stores before staging the second half
@@ -492,27 +491,54 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     __syncthreads();
 
     if (dZ != nullptr) {
-#pragma unroll 4
-      for (int rr = 0; rr < 16; ++rr) {
-        const int n = wave * 16 + rr;
-        const int tl = 128 * h + n;  // token row within the tile
-        if (n0 + tl >= rows) break;
-        const f32x4_t z = *reinterpret_cast<const f32x4_t*>(st + n * 256 + ((lane ^ hsw16(n)) << 2));
-        const uint32_t mark = (hbits[n * 8 + (lane >> 3)] >> ((lane & 7) * 4)) & 15u;
-        const float cm = rs_cm[tl], L2 = rs_l2[tl];
-        f32x4_t G;
+      // The wave's 16 rows go in two batches of 8 whose LDS reads are all
+      // issued before their arithmetic. The row pass is VALU-bound (every
+      // element costs an exp2), so it carries no per-element selects: a row's
+      // teacher cells (about one row in five has any) are substituted behind
+      // a wave-uniform test, and columns past V get no mask (their z is
+      // exactly 0, as W's rows past V read as zeros, so they hold finite
+      // values that only ever meet those zero rows).
+      const int rb = wave * 16;                                      // first row in the half
+      const int nrow = max(0, min(16, rows - (n0 + 128 * h + rb)));  // rows that exist
+      {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ok = vfull || (m0 + vl0 + e < V);
-          const float dense = ok ? cm * fast_exp2(z[e] * k2 - L2) : 0.f;
-          G[e] = (mark >> e) & 1u ? z[e] : dense;
-        }
-        T* dst = dZ + (int64_t)(n0 + tl) * ldz + m0 + vl0;
-        if constexpr (sizeof(T) == 2) {
-          u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
-          *reinterpret_cast<u32x2_t*>(dst) = pk2;
-        } else {
-          *reinterpret_cast<f32x4_t*>(dst) = G;
+        for (int b8 = 0; b8 < 16; b8 += 8) {
+          f32x4_t zr[8];
+          uint32_t mk[8];
+#pragma unroll
+          for (int rr = 0; rr < 8; ++rr) {
+            const int n = rb + b8 + rr;
+            zr[rr] = *reinterpret_cast<const f32x4_t*>(st + n * 256 + ((lane ^ hsw16(n)) << 2));
+            mk[rr] = (hbits[n * 8 + (lane >> 3)] >> ((lane & 7) * 4)) & 15u;
+          }
+          f32x4_t cmv[2], l2v[2];  // the rows' g/tau M and log2 Z (16-byte aligned runs)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            cmv[u] = *reinterpret_cast<const f32x4_t*>(rs_cm + 128 * h + rb + b8 + 4 * u);
+            l2v[u] = *reinterpret_cast<const f32x4_t*>(rs_l2 + 128 * h + rb + b8 + 4 * u);
+          }
+#pragma unroll
+          for (int rr = 0; rr < 8; ++rr) {
+            const float cm = cmv[rr >> 2][rr & 3], L2 = l2v[rr >> 2][rr & 3];
+            f32x4_t G;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) G[e] = cm * fast_exp2(zr[rr][e] * k2 - L2);
+            if (__builtin_amdgcn_ballot_w64(mk[rr] != 0u) != 0ull) {
+              // teacher cells hold their final value (patched by the fold)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if ((mk[rr] >> e) & 1u) G[e] = zr[rr][e];
+            }
+            if (b8 + rr < nrow) {
+              T* dst = dZ + (int64_t)(n0 + 128 * h + rb + b8 + rr) * ldz + m0 + vl0;
+              if constexpr (sizeof(T) == 2) {
+                u32x2_t pk2 = {pack_bf16x2(G[0], G[1]), pack_bf16x2(G[2], G[3])};
+                *reinterpret_cast<u32x2_t*>(dst) = pk2;
+              } else {
+                *reinterpret_cast<f32x4_t*>(dst) = G;
+              }
+            }
+          }
         }
       }
     }

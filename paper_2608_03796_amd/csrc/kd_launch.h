@@ -45,7 +45,7 @@ struct KdChunkArgs {
   int* hoff;                // [cdiv(rows, 256), nVT + 1] bucket offsets
   float* zhit;              // [rows, K] student logit at each teacher entry
   void* dZ;                 // this chunk's rows of the group's dZ [rows, ldz]
-  int64_t ldz;              // = padded vocabulary (columns V..ldz are written as 0)
+  int64_t ldz;              // = padded vocabulary (columns V..ldz: finite, z = 0 there)
   int dh_split;
   float* dh_partial;        // [dh_split, rows, D] when dh_split > 1
   // outputs
