@@ -12,6 +12,7 @@
 // Per group of chunks: dw        -> grad_W (+)= dZ^T H (fp32 accumulate)
 // Per call:    finalize_loss     -> mean over non-ignored tokens
 #include "kd_device.h"
+#include <type_traits>
 #include "kd_launch.h"
 
 #include <string.h>
@@ -210,40 +211,47 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
   }
   float* xch = reinterpret_cast<float*>(lds);  // [wn][j][16 lanes][max, sum]
   float rm[4], rs[4];
+  // Per token: the max is taken over z itself (k2 > 0), then sum 2^(z k2 - max)
+  // (one fma, one exp2 and one add per element). Only the last vocabulary
+  // tile of a V that is not a multiple of 256 tests its columns.
+  auto lse = [&](auto full_tile) {
+    constexpr bool kFull = decltype(full_tile)::value;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int v = m0 + acc_m(wm, i, lane, r);
-        const float y = acc.v[i][j][r] * k2;
-        if (full || v < V) mx = fmaxf(mx, y);
-      }
-    // the four lane groups (lane>>4) hold the other rows of the same token
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    float s = 0.f;
-    if (mx != -INFINITY) {
+    for (int j = 0; j < 4; ++j) {
+      float za = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int v = m0 + acc_m(wm, i, lane, r);
-          const float e = fast_exp2(acc.v[i][j][r] * k2 - mx);
-          if (full || v < V) s += e;
-        }
+        for (int r = 0; r < 4; ++r)
+          if (kFull || m0 + acc_m(wm, i, lane, r) < V) za = fmaxf(za, acc.v[i][j][r]);
+      // the four lane groups (lane>>4) hold the other rows of the same token
+      za = fmaxf(za, __shfl_xor(za, 16));
+      za = fmaxf(za, __shfl_xor(za, 32));
+      const float mx = za * k2;
+      float s = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = fast_exp2(acc.v[i][j][r] * k2 - mx);
+            if (kFull || m0 + acc_m(wm, i, lane, r) < V) s += e;
+          }
+      }
+      s += __shfl_xor(s, 16);
+      s += __shfl_xor(s, 32);
+      rm[j] = mx;
+      rs[j] = s;
+      if (wm == 1 && lane < 16) {
+        xch[((wn * 4 + j) * 16 + lane) * 2 + 0] = mx;
+        xch[((wn * 4 + j) * 16 + lane) * 2 + 1] = s;
+      }
     }
-    s += __shfl_xor(s, 16);
-    s += __shfl_xor(s, 32);
-    rm[j] = mx;
-    rs[j] = s;
-    if (wm == 1 && lane < 16) {
-      xch[((wn * 4 + j) * 16 + lane) * 2 + 0] = mx;
-      xch[((wn * 4 + j) * 16 + lane) * 2 + 1] = s;
-    }
-  }
+  };
+  if (full)
+    lse(std::integral_constant<bool, true>());
+  else
+    lse(std::integral_constant<bool, false>());
   __syncthreads();
   if (wm == 0 && lane < 16) {
 #pragma unroll
