@@ -47,7 +47,7 @@ extern "C" {
 typedef enum kd_status {
   KD_OK = 0,
   KD_ERR_NULL_PTR = 1,           /* a required pointer is NULL */
-  KD_ERR_BAD_SHAPE = 2,          /* N < 0, D/V/K <= 0, K > V, or a size limit */
+  KD_ERR_BAD_SHAPE = 2,          /* N < 0, D/V/K <= 0, K > V, K > 4096, or a size limit */
   KD_ERR_BAD_ARG = 3,            /* chunk <= 0, tau not finite or <= 0, flags */
   KD_ERR_UNSUPPORTED = 4,        /* dtype, D % 64 != 0, misaligned pointer */
   KD_ERR_WORKSPACE_TOO_SMALL = 5,
@@ -66,7 +66,7 @@ typedef struct kd_problem {
   int64_t D;           /* hidden size d; 64 <= D <= 65536, D % 64 == 0       */
   int64_t V;           /* vocabulary size; 1 <= V <= 1048576                 */
   int64_t chunk;       /* rows per chunk C_s; >= 1 (min(chunk, N) is used)   */
-  int32_t K;           /* cached teacher entries per token; 1 <= K <= V      */
+  int32_t K;           /* cached teacher entries per token; 1 <= K <= V, K <= 4096 */
   int32_t dtype;       /* kd_dtype of hidden, W and grad_hidden              */
   float temperature;   /* tau; finite and > 0                                */
   int32_t flags;       /* 0 or KD_FLAG_TEACHER_LOGPROBS                      */

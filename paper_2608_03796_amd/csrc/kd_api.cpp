@@ -17,6 +17,9 @@ constexpr int64_t kMaxN = (int64_t)1 << 31;     // N < 2^31
 constexpr int64_t kMaxV = (int64_t)1 << 20;     // keeps 32-bit buffer offsets in range
 constexpr int64_t kMaxD = 65536;
 constexpr int64_t kMaxChunk = (int64_t)1 << 20; // rows per chunk actually used
+// teacher entries per token: a 256-token tile's 256 K entries are numbered in
+// 20 bits by the bucket pass, and k is packed in 16
+constexpr int64_t kMaxK = 4096;
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t rup(int64_t a, int64_t b) { return cdiv(a, b) * b; }
@@ -44,7 +47,7 @@ kd_status check_problem(const kd_problem* p) {
   if (p->N < 0 || p->N >= kMaxN) return KD_ERR_BAD_SHAPE;
   if (p->D < 64 || p->D > kMaxD) return KD_ERR_BAD_SHAPE;
   if (p->V < 1 || p->V > kMaxV) return KD_ERR_BAD_SHAPE;
-  if (p->K < 1 || (int64_t)p->K > p->V) return KD_ERR_BAD_SHAPE;
+  if (p->K < 1 || (int64_t)p->K > p->V || p->K > kMaxK) return KD_ERR_BAD_SHAPE;
   if (p->chunk < 1) return KD_ERR_BAD_ARG;
   if (!(isfinite(p->temperature) && p->temperature > 0.0f)) return KD_ERR_BAD_ARG;
   if (p->D % 64 != 0) return KD_ERR_UNSUPPORTED;

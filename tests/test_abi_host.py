@@ -61,7 +61,7 @@ def _ws(lib, pr):
 @pytest.mark.parametrize("kw,code", [
     (dict(N=-1), 2), (dict(N=2 ** 31), 2), (dict(D=0), 2), (dict(D=32), 2), (dict(D=65600), 2),
     (dict(D=96), 4), (dict(V=0), 2), (dict(V=2 ** 20 + 1), 2), (dict(K=0), 2),
-    (dict(K=4097), 2), (dict(chunk=0), 3), (dict(chunk=-5), 3), (dict(tau=0.0), 3),
+    (dict(K=4097), 2), (dict(V=65536, K=4097), 2), (dict(chunk=0), 3), (dict(chunk=-5), 3), (dict(tau=0.0), 3),
     (dict(tau=-1.0), 3), (dict(tau=float("inf")), 3), (dict(tau=float("nan")), 3),
     (dict(dtype=2), 4), (dict(dtype=-1), 4), (dict(flags=2), 3), (dict(flags=-1), 3),
 ])

@@ -70,6 +70,15 @@ def test_k_equals_v(gpu_lib):
     _run_and_compare(gpu_lib, inp, 1.0, 32, TOL["f32"])
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_k_at_the_limit(gpu_lib, dtype):
+    """K = 4096, the largest accepted: a 256-token tile carries 2^20 teacher
+    entries through the bucket pass (ragged second tile, 5000-column V)."""
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(260, 64, 5000, 4096, tdt, seed=41)
+    _run_and_compare(gpu_lib, inp, 1.3, 130, TOL[dtype])
+
+
 def test_identity_head_kl_zero(gpu_lib):
     """W = I (D = V): hidden are the logits; teacher reproduced on its support
     and -1e4 elsewhere gives l = 0 and zero gradients (P2)."""
