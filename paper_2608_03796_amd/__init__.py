@@ -123,9 +123,13 @@ def alloc_workspace(N, D, V, K, chunk, tau, dtype, device):
 
 
 def _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore):
+    """Dtypes, shapes, devices and layouts of the inputs. The library takes
+    plain pointers, so every size it will index with is checked here."""
     import torch
     if hidden.device.type != "cuda":
         raise ValueError("tensors must be on a GPU")
+    if hidden.dim() != 2 or W.dim() != 2:
+        raise ValueError("hidden must be [N, D] and W [V, D]")
     if W.dtype != hidden.dtype:
         raise TypeError("hidden and W must share a dtype")
     for name, t, want in (("teacher_idx", teacher_idx, torch.int32),
@@ -134,13 +138,38 @@ def _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore):
             raise TypeError(f"{name} must be {want}")
     if ignore is not None and ignore.dtype != torch.uint8:
         raise TypeError("ignore must be uint8")
+    N, D = hidden.shape
+    if W.shape[1] != D:
+        raise ValueError(f"W is {tuple(W.shape)}, expected [V, {D}]")
+    if teacher_idx.dim() != 2 or teacher_idx.shape[0] != N:
+        raise ValueError(f"teacher_idx is {tuple(teacher_idx.shape)}, expected [{N}, K]")
+    K = teacher_idx.shape[1]
+    if tuple(teacher_logit.shape) != (N, K):
+        raise ValueError(f"teacher_logit is {tuple(teacher_logit.shape)}, expected [{N}, {K}]")
+    if ignore is not None and tuple(ignore.shape) != (N,):
+        raise ValueError(f"ignore is {tuple(ignore.shape)}, expected [{N}]")
     tensors = [hidden, W, teacher_idx, teacher_logit] + ([ignore] if ignore is not None else [])
     for t in tensors:
         if not t.is_contiguous():
             raise ValueError("inputs must be contiguous")
-    N, D = hidden.shape
-    K = teacher_idx.shape[1] if teacher_idx.dim() == 2 else 0
+        if t.device != hidden.device:
+            raise ValueError("inputs must be on one device")
     return N, D, W.shape[0], K, _dtype_code(hidden.dtype)
+
+
+def _check_tensor(name, t, shape, dtype, device):
+    """A caller-provided output or extra input: exact shape, dtype, device, layout."""
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype or t.device != device \
+            or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)} "
+                         f"on {device} (got {t.dtype} {tuple(t.shape)} on {t.device})")
+
+
+def _check_workspace(workspace, device):
+    import torch
+    if workspace.dtype != torch.uint8 or workspace.device != device \
+            or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor on the inputs' device")
 
 
 def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
@@ -172,15 +201,24 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
             out["grad_W"] = grad_W_out
         elif "grad_W" not in out:
             out["grad_W"] = torch.empty(V, D, dtype=torch.float32, device=dev)
+    _check_tensor("loss", out["loss"], (), torch.float32, dev)
+    if loss_per_token:
+        _check_tensor("loss_per_token", out["loss_per_token"], (N,), torch.float32, dev)
+    if grad_hidden:
+        _check_tensor("grad_hidden", out["grad_hidden"], (N, D), hidden.dtype, dev)
+    if grad_W:
+        _check_tensor("grad_W", out["grad_W"], (V, D), torch.float32, dev)
     pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
-    rc = lib.kd_topk_kl_fwd_bwd(
-        ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
-        _ptr(ignore), _ptr(out["loss"]), _ptr(out.get("loss_per_token") if loss_per_token else None),
-        _ptr(out.get("grad_hidden") if grad_hidden else None),
-        _ptr(out.get("grad_W") if grad_W else None), int(bool(accumulate_grad_W)),
-        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
+    _check_workspace(workspace, dev)
+    with torch.cuda.device(dev):
+        rc = lib.kd_topk_kl_fwd_bwd(
+            ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+            _ptr(ignore), _ptr(out["loss"]), _ptr(out.get("loss_per_token") if loss_per_token else None),
+            _ptr(out.get("grad_hidden") if grad_hidden else None),
+            _ptr(out.get("grad_W") if grad_W else None), int(bool(accumulate_grad_W)),
+            _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
     if rc != 0:
         raise KdError(rc, "kd_topk_kl_fwd_bwd")
     res = {"loss": out["loss"]}
@@ -210,10 +248,12 @@ def fwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
     pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
-    rc = lib.kd_topk_kl_fwd(
-        ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
-        _ptr(ignore), _ptr(res["loss"]), _ptr(res.get("loss_per_token")), _ptr(res["saved_logz"]),
-        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
+    _check_workspace(workspace, dev)
+    with torch.cuda.device(dev):
+        rc = lib.kd_topk_kl_fwd(
+            ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+            _ptr(ignore), _ptr(res["loss"]), _ptr(res.get("loss_per_token")), _ptr(res["saved_logz"]),
+            _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
     if rc != 0:
         raise KdError(rc, "kd_topk_kl_fwd")
     return res
@@ -231,24 +271,30 @@ def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ign
     lib = load_library()
     N, D, V, K, dt = _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore)
     dev = hidden.device
-    for name, t in (("saved_logz", saved_logz), ("grad_loss", grad_loss),
-                    ("grad_loss_per_token", grad_loss_per_token)):
-        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous()):
-            raise TypeError(f"{name} must be a contiguous fp32 tensor")
+    _check_tensor("saved_logz", saved_logz, (N,), torch.float32, dev)
+    if grad_loss is not None and grad_loss.numel() == 1:
+        _check_tensor("grad_loss", grad_loss, tuple(grad_loss.shape), torch.float32, dev)
+    elif grad_loss is not None:
+        raise ValueError("grad_loss must hold one value (the upstream gradient of the mean)")
+    if grad_loss_per_token is not None:
+        _check_tensor("grad_loss_per_token", grad_loss_per_token, (N,), torch.float32, dev)
     res = {}
     if grad_hidden:
         res["grad_hidden"] = torch.empty(N, D, dtype=hidden.dtype, device=dev)
     if grad_W:
         res["grad_W"] = grad_W_out if grad_W_out is not None else torch.empty(
             V, D, dtype=torch.float32, device=dev)
+        _check_tensor("grad_W", res["grad_W"], (V, D), torch.float32, dev)
     pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
-    rc = lib.kd_topk_kl_bwd(
-        ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
-        _ptr(ignore), _ptr(saved_logz), _ptr(grad_loss), _ptr(grad_loss_per_token),
-        _ptr(res.get("grad_hidden")), _ptr(res.get("grad_W")), int(bool(accumulate_grad_W)),
-        _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
+    _check_workspace(workspace, dev)
+    with torch.cuda.device(dev):
+        rc = lib.kd_topk_kl_bwd(
+            ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+            _ptr(ignore), _ptr(saved_logz), _ptr(grad_loss), _ptr(grad_loss_per_token),
+            _ptr(res.get("grad_hidden")), _ptr(res.get("grad_W")), int(bool(accumulate_grad_W)),
+            _ptr(workspace), ctypes.c_size_t(workspace.numel()), _stream_handle(dev))
     if rc != 0:
         raise KdError(rc, "kd_topk_kl_bwd")
     return res
@@ -307,14 +353,20 @@ def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore
 
 def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, workspace=None):
     """True if every index is in [0, V) and no row repeats one (synchronises)."""
+    import torch
     lib = load_library()
+    if teacher_idx.device.type != "cuda" or teacher_idx.dtype != torch.int32 \
+            or teacher_idx.dim() != 2 or not teacher_idx.is_contiguous():
+        raise ValueError("teacher_idx must be a contiguous [N, K] int32 GPU tensor")
     N, K = teacher_idx.shape
     pr = problem(N, D, V, K, chunk, tau, dtype)
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dtype, teacher_idx.device)
-    rc = lib.kd_topk_kl_check_indices(ctypes.byref(pr), _ptr(teacher_idx), _ptr(workspace),
-                                      ctypes.c_size_t(workspace.numel()),
-                                      _stream_handle(teacher_idx.device))
+    _check_workspace(workspace, teacher_idx.device)
+    with torch.cuda.device(teacher_idx.device):
+        rc = lib.kd_topk_kl_check_indices(ctypes.byref(pr), _ptr(teacher_idx), _ptr(workspace),
+                                          ctypes.c_size_t(workspace.numel()),
+                                          _stream_handle(teacher_idx.device))
     if rc == 6:
         return False
     if rc != 0:
