@@ -820,7 +820,10 @@ struct ProfScope {
     if (!a) return;
     std::lock_guard<std::mutex> g(g_prof_mu);
     hipEvent_t b = prof_event();
-    if (!b) return;
+    if (!b) {
+      g_prof_pool.push_back(a);  // no pair: drop this record, keep the event
+      return;
+    }
     (void)hipEventRecord(b, s);
     g_prof_recs.push_back({kind, a, b, flops});
   }
