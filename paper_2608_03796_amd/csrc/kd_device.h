@@ -134,9 +134,10 @@ __device__ __forceinline__ int acc_n(int wn, int j, int lane) {
 //    gets element i%4 of the 8 bytes addressed by lane 4k + i/4 as its value
 //    k), so W, dZ and the hidden rows are consumed where they are.
 // Operands go straight from memory into LDS (buffer loads with the LDS-DMA
-// bit) through S stages of 32 KiB per operand; one barrier per K step; the
-// next sub-step's fragments are read while the current sub-step's MFMAs run.
-// The caller's LDS must hold kLdsMain bytes; ends with a barrier.
+// bit) through stages of 32 KiB per operand (two per operand, or three for A
+// and two for B); one barrier per K step; the next sub-step's fragments are
+// read while the current sub-step's MFMAs run. The caller's LDS must hold
+// kLdsMain bytes (kLdsA3 with SA = 3); ends with a barrier.
 //
 // The DMA loads are issued from inline assembly, so the compiler does not
 // track them: it would otherwise make every transposing LDS read wait for all
@@ -147,6 +148,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4_t;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int kLdsMain = kStages * 2 * kTile * kRowB;  // 128 KiB
+constexpr int kLdsA3 = 5 * kTile * kRowB;              // 160 KiB: 3 A stages + 2 B stages
 
 struct KcOp {
   const char* base;
@@ -358,11 +360,13 @@ struct OpFrag<float, KmOp, NB> {
 };
 
 // SPREAD selects the fragment-read placement: false puts sub-step 1's reads
-// under the compiler's MFMA/read interleave and sub-step 0's reads on the
-// first pairs of the second half; true places both by hand, fragment f with
-// pair f * NP / (8 + NJ). Which one is faster depends on the operand layouts
-// (measured per kernel).
-template <typename T, typename OA, typename OB, int NW = 8, bool SPREAD = false>
+// under the compiler's MFMA/read interleave (by hand, one per pair, with
+// SA = 3) and sub-step 0's reads on the first pairs of the second half; true
+// places both by hand, fragment f with pair f * NP / (8 + NJ). Which one is
+// faster depends on the operand layouts (measured per kernel). SA is the
+// number of A stages: 2 (all DMA of a step in its second half) or 3 (the DMA
+// split between the halves; 160 KiB of LDS).
+template <typename T, typename OA, typename OB, int NW = 8, bool SPREAD = false, int SA = 2>
 __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_begin, int ks_end,
                                           char* lds, AccTileT<WaveGrid<NW>::NJ>& acc) {
   typedef WaveGrid<NW> WG;
@@ -414,6 +418,86 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
     acc.v[i][j] = mfma_slot(fa[i], fb[j], acc.v[i][j], (T*)nullptr);
     acc.v[i][j + 1] = mfma_slot(fa[i], fb[j + 1], acc.v[i][j + 1], (T*)nullptr);
   };
+
+  if constexpr (SA == 3) {
+    // Three A stages and two B stages (160 KiB): step k's A operand lives in
+    // A stage k % 3 and its B operand in B stage k % 2. Step j+2's A DMA goes
+    // out during step j's first half (into the A stage retired at barrier
+    // j-1), its B DMA during step j's second half (into the B stage retired at
+    // barrier j), so each half issues half of the step's DMA (the per-CU
+    // DMA issue rate is what limited the half that carried all of it) and the
+    // A half has ~1.4 steps to land; both are waited for at barrier j+1. The
+    // instructions go on every fourth MFMA pair, A's on pairs 3, 7, 11, 15 and
+    // B's on pairs 0, 4, 8, 12 (measured best of the placements tried).
+    constexpr int DS = NP / NPW;  // pairs per DMA instruction
+    char* const lb = lds + 3 * OPB;
+    auto aS = [&](int k3) { return lds + k3 * OPB; };
+    auto bS = [&](int k2) { return lb + k2 * OPB; };
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const bool live = ks_begin + p < ks_end;
+      const DmaStep<NPW> sa = da.prep(opa, aS(p), wave, ks_begin + p, live);
+      const DmaStep<NPW> sb = db.prep(opb, bS(p), wave, ks_begin + p, live);
+#pragma unroll
+      for (int i = 0; i < NPW; ++i) sa.one(i);
+#pragma unroll
+      for (int i = 0; i < NPW; ++i) sb.one(i);
+    }
+    KD_VMCNT(NI);
+    __syncthreads();
+    u32x4_t fa[2][8], fb[2][NJ];
+#pragma unroll
+    for (int b = 0; b < 8; ++b) fa[0][b] = fra.one(aS(0), 0, b);
+#pragma unroll
+    for (int b = 0; b < NJ; ++b) fb[0][b] = frb.one(bS(0), 0, b);
+    constexpr int NF3 = 8 + NJ;
+    auto read3 = [&](int q, const char* a, const char* b, int s, u32x4_t (&xa)[8],
+                     u32x4_t (&xb)[NJ]) {
+#pragma unroll
+      for (int f = 0; f < NF3; ++f)
+        if ((SPREAD ? (f * NP) / NF3 : f) == q) {
+          if (f < 8) xa[f] = fra.one(a, s, f);
+          else xb[f - 8] = frb.one(b, s, f - 8);
+        }
+    };
+    int ca = 0, cb = 0;  // A and B stages of step j
+    for (int j = 0; j < nsteps; ++j) {
+      const int ks = ks_begin + j + 2;
+      {
+        const DmaStep<NPW> sa = da.prep(opa, aS(ca == 0 ? 2 : ca - 1), wave, ks, ks < ks_end);
+        const char* a = aS(ca);
+        const char* b = bS(cb);
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          if (q % DS == DS - 1) sa.one(q / DS);
+          mfma2(q, fa[0], fb[0]);
+          read3(q, a, b, 1, fa[1], fb[1]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f & ~0x0f00);  // lgkmcnt(0)
+      KD_VMCNT(NPW);  // step j+1 landed; step j+2's A DMA may still fly
+      __syncthreads();
+      const int na = ca == 2 ? 0 : ca + 1, nb = cb ^ 1;
+      {
+        const DmaStep<NPW> sb = db.prep(opb, bS(cb), wave, ks, ks < ks_end);
+        const char* a = aS(na);
+        const char* b = bS(nb);
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          if (q % DS == 0) sb.one(q / DS);
+          mfma2(q, fa[1], fb[1]);
+          read3(q, a, b, 0, fa[0], fb[0]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      ca = na;
+      cb = nb;
+    }
+    KD_VMCNT(0);
+    __syncthreads();
+    return;
+  }
 
   // Step j lives in stage j % S; S steps of DMA are always in flight. Sub-step
   // 0's MFMAs run interleaved with the reads of sub-step 1's fragments; then

@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
                                                             const uint32_t* __restrict__ hits,
                                                             const int* __restrict__ hoff, int K,
                                                             float* zhit) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
+  __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
@@ -132,9 +132,10 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
   const int ld = D * eb;
   const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
   AccTile acc;
-  gemm_tile<T>(KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
-               KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld},
-               0, ld / kRowB, lds, acc);
+  gemm_tile<T, KcOp, KcOp, 8, false, 3>(
+      KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
+      KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld}, 0,
+      ld / kRowB, lds, acc);
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
@@ -615,7 +616,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
                                                     const T* __restrict__ W, int V, int rows,
                                                     int D, int TM, int TN, int ks_total,
                                                     int split, T* gH, float* partial) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
+  __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   const int tiles = TM * TN;
   const int sidx = blockIdx.x / tiles;
   int mt, nt;
@@ -627,7 +628,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const int kb = sidx * per, ke = min(ks_total, kb + per);
   AccTile acc;
   const int mrows = min(kTile, rows - m0);
-  gemm_tile<T, KcOp, KmOp, 8, true>(
+  gemm_tile<T, KcOp, KmOp, 8, true, 3>(
       KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
                KmOp{reinterpret_cast<const char*>(W + n0),
                     (int64_t)V * ldb - (int64_t)n0 * eb, ldb},
@@ -673,7 +674,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, in
                                                     const T* __restrict__ Hg, int tokens, int V,
                                                     int D, int TM, int TN, int beta,
                                                     float* __restrict__ gW) {
-  __shared__ __attribute__((aligned(16))) char lds[kLdsMain];
+  __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
@@ -682,7 +683,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, in
   const int mrows = min(kTile, V - m0);
   constexpr int KS = kRowB / (int)sizeof(T);
   AccTile acc;
-  gemm_tile<T>(KmOp{reinterpret_cast<const char*>(dZ + m0), (int64_t)tokens * lda - (int64_t)m0 * eb, lda},
+  gemm_tile<T, KmOp, KmOp, 8, false, 3>(
+      KmOp{reinterpret_cast<const char*>(dZ + m0), (int64_t)tokens * lda - (int64_t)m0 * eb, lda},
                KmOp{reinterpret_cast<const char*>(Hg + n0), (int64_t)tokens * ldb - (int64_t)n0 * eb, ldb},
                0, (tokens + KS - 1) / KS, lds, acc);
   // Output tile in two halves of 128 rows: the waves holding a half stage it
