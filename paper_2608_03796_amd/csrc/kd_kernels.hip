@@ -393,9 +393,10 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __rest
 
 // --------------------------------------- logit recompute + dZ epilogue -----
 // Same tile as k_logits_lse (bitwise identical z). Before the main loop the
-// tile's per-token scalars (g/tau M, g/tau, log2 Z) and its bucket of teacher
-// entries are copied into spare LDS by DMA, so the epilogue issues no global
-// loads (a load waited for after a store would also wait for that store).
+// tile's per-token scalars (g/tau M, g/tau, log2 Z) and its teacher entries
+// (one per thread) are loaded into registers, so the epilogue issues no
+// global loads (a load waited for after a store would also wait for that
+// store); after the loop the scalars go to LDS beside the staging area.
 // The fp32 tile is staged 128 tokens at a time as [token][vocab] with a
 // 16-byte-slot swizzle; each teacher entry of the half is patched in place to
 // its final value (g/tau)(M q - p), its z is recorded for C, and a bitmap marks
@@ -403,11 +404,10 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __rest
 // stores the row of dZ[rows, Vp] (columns V..Vp as zeros).
 __device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
 
-constexpr int kDzRows = kLdsMain;             // 3 x 256 floats: g/tau M, g/tau, log2 Z
-constexpr int kDzHits = kDzRows + 3 * 1024;   // kDzHitCap entries, then their p
-constexpr int kDzHitCap = 512;
-constexpr int kDzBits = kDzHits + 8 * kDzHitCap;  // 128 x 256-bit hit map of one half
-constexpr int kDzLds = kDzBits + 4 * 1024;
+// epilogue LDS (the main loop's stages are free by then): staging [0, 128 KiB)
+constexpr int kDzBits = kLdsMain;              // 128 x 256-bit hit map of one half
+constexpr int kDzRows = kDzBits + 4 * 1024;    // 3 x 256 floats: g/tau M, g/tau, log2 Z
+static_assert(kDzRows + 3 * 1024 <= kLdsA3, "dZ epilogue LDS");
 
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_dz(
@@ -416,7 +416,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     const float* __restrict__ rowCoefM, const uint32_t* __restrict__ hits,
     const float* __restrict__ hitp, const int* __restrict__ hoff, int K, int nVT, T* dZ,
     int64_t ldz, float* zhit) {
-  __shared__ __attribute__((aligned(16))) char lds[kDzLds];
+  __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
@@ -430,35 +430,42 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   const int64_t seg = (int64_t)nt * kTile * K;
   const int* ho = hoff + (int64_t)nt * (nVT + 1) + mt;
   const int hb = ho[0], cnt = ho[1] - hb;
-  if (wave < 3) {
-    const float* src = wave == 0 ? rowCoefM : wave == 1 ? rowCoef : rowL2;
-    dma_b128(rsrc_words(src + n0, (uint32_t)nrows * 4u),
-             __builtin_amdgcn_readfirstlane(lds_addr(lds + kDzRows + wave * 1024)), lane * 16);
-  } else if (wave < 7) {
-    // waves 3, 4: entries [0, 256), [256, 512); waves 5, 6: their p
-    const int part = (wave - 3) & 1;
-    const char* src = wave < 5 ? reinterpret_cast<const char*>(hits + seg)
-                               : reinterpret_cast<const char*>(hitp + seg);
-    const i32x4_t r = rsrc_words(src, (uint32_t)(hb + cnt) * 4u);
-    const uint32_t la = __builtin_amdgcn_readfirstlane(
-        lds_addr(lds + kDzHits + (wave < 5 ? 0 : 4 * kDzHitCap) + part * 1024));
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      dma_b32(r, la + q * 256, (uint32_t)(hb + part * 256 + q * 64 + lane) * 4u);
+  // wave w holds the scalars of tokens [32 w, 32 w + 32): lane l has token
+  // 32 w + (l & 31), g/tau M and g/tau (l < 32) or log2 Z (l >= 32, in rv0)
+  float rv0, rv1 = 0.f;
+  {
+    const int t = n0 + 32 * wave + (lane & 31);
+    const bool ok = t < rows;
+    rv0 = ok ? (lane < 32 ? rowCoefM[t] : rowL2[t]) : 0.f;
+    if (lane < 32) rv1 = ok ? rowCoef[t] : 0.f;
+  }
+  uint32_t fe = 0u;  // this thread's teacher entry (entry tid of the bucket) and its p
+  float fpk = 0.f;
+  if (tid < cnt) {
+    fe = hits[seg + hb + tid];
+    fpk = hitp[seg + hb + tid];
   }
 
   AccTile acc;
-  gemm_tile<T>(KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
-               KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld},
-               0, ld / kRowB, lds, acc);
-  KD_VMCNT(0);  // the prefetch above (published by the first barrier below)
+  gemm_tile<T, KcOp, KcOp, 8, false, 3>(
+      KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
+      KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld}, 0,
+      ld / kRowB, lds, acc);
+  {
+    float* rs = reinterpret_cast<float*>(lds + kDzRows);
+    const int t = 32 * wave + (lane & 31);
+    if (lane < 32) {
+      rs[t] = rv0;
+      rs[256 + t] = rv1;
+    } else {
+      rs[512 + t] = rv0;
+    }
+  }
 
   float* st = reinterpret_cast<float*>(lds);
   const float* rs_cm = reinterpret_cast<const float*>(lds + kDzRows);
   const float* rs_cf = rs_cm + 256;
   const float* rs_l2 = rs_cm + 512;
-  const uint32_t* hl = reinterpret_cast<const uint32_t*>(lds + kDzHits);
-  const float* hp = reinterpret_cast<const float*>(lds + kDzHits + 4 * kDzHitCap);
   uint32_t* hbits = reinterpret_cast<uint32_t*>(lds + kDzBits);
   const int vl0 = 4 * lane;  // this lane's 4 vocabulary columns in the row pass
 
@@ -482,9 +489,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     __syncthreads();
 
     // Teacher entries of this half: dZ = (g/tau) M q - (g/tau) p in place,
-    // z kept for C = sum_k p z (Eq. 2). The first kDzHitCap entries come from
-    // the LDS copy; a skewed teacher with more entries in one tile reads the
-    // rest from memory.
+    // z kept for C = sum_k p z (Eq. 2). Thread tid has entry tid of the
+    // bucket in registers; a skewed teacher with more entries in one tile
+    // than threads reads the rest from memory.
     auto fold = [&](uint32_t e, float pk) {
       const int tl = (int)(e & 255u);
       if ((tl >> 7) != h) return;
@@ -495,8 +502,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
       *cell = rs_cm[tl] * fast_exp2(z * k2 - rs_l2[tl]) - rs_cf[tl] * pk;
       atomicOr(&hbits[n * 8 + (v >> 5)], 1u << (v & 31));
     };
-    for (int q = tid; q < min(cnt, kDzHitCap); q += kThreads) fold(hl[q], hp[q]);
-    for (int q = kDzHitCap + tid; q < cnt; q += kThreads) fold(hits[seg + hb + q], hitp[seg + hb + q]);
+    if (tid < cnt) fold(fe, fpk);
+    // a bucket with more entries than threads: the rest from memory
+    for (int q = kThreads + tid; q < cnt; q += kThreads) fold(hits[seg + hb + q], hitp[seg + hb + q]);
     __syncthreads();
 
     if (dZ != nullptr) {
