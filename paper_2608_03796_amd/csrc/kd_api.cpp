@@ -37,7 +37,7 @@ struct Plan {
   int64_t G;           // chunks whose dZ rows are gathered before one dW GEMM
   int dh_split;
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
-      off_lossp, off_dz, off_dhs, total;
+      off_lossp, off_dz, off_ht, off_dhs, total;
 };
 
 kd_status check_problem(const kd_problem* p) {
@@ -108,6 +108,8 @@ Plan make_plan(const kd_problem* p) {
   pl.off_zhit = take((size_t)pl.cp * pl.K * 4);
   pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
   pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
+  // the hidden rows of one dW group, transposed (tokens padded to 64)
+  pl.off_ht = take((size_t)pl.D * rup(pl.G * pl.c, 64) * pl.eb);
   pl.off_dhs = pl.dh_split > 1 ? take((size_t)pl.dh_split * pl.c * pl.D * 4) : 0;
   pl.total = align256(t);
   return pl;
@@ -264,6 +266,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       d.ldz = pl.Vp;
       d.Hg = static_cast<const char*>(c.hidden) + (row0 + rcount - group_tokens) * pl.D * pl.eb;
       d.tokens = group_tokens;
+      d.Ht = ws + pl.off_ht;
       d.beta = (dw_done || c.accumulate) ? 1 : 0;
       d.gW = c.grad_W;
       if (kd_launch_dw(&d, c.stream) != 0) return KD_ERR_DEVICE;

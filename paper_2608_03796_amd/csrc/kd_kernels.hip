@@ -674,83 +674,129 @@ __global__ void k_dh_reduce(const float* partial, int split, int64_t n, T* gH) {
 }
 
 // -------------------------------------------------------------------- dW ----
-// grad_W[v, d] (+)= sum_t dZ[t, v] H[t, d] over the tokens of a group of
-// chunks: both operands read K-major (rows = tokens), token rows past the
-// group read as zeros; fp32 read-modify-write of the output tile when beta = 1.
+// The group's hidden rows transposed: Ht[d, t] = H[t, d] for t < tokens and 0
+// for tokens <= t < ldt (ldt a multiple of 64), so that the dW contraction
+// reads them with the tokens (its K dimension) contiguous. One 64 x 64 block
+// per workgroup, 16-byte loads and stores on both sides.
 template <typename T>
-__global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ dZ, int64_t ldz,
-                                                    const T* __restrict__ Hg, int tokens, int V,
-                                                    int D, int TM, int TN, int beta,
-                                                    float* __restrict__ gW) {
+__global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H, int tokens,
+                                                         int D, T* __restrict__ Ht, int ldt) {
+  constexpr int VPT = 16 / (int)sizeof(T);      // elements per 16-byte piece
+  constexpr int PAD = 4 / (int)sizeof(T);       // one dword of padding per LDS row
+  __shared__ T tile[64][64 + PAD];              // [token][feature]
+  const int t0 = blockIdx.x * 64, d0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < 64 * 64 / VPT / 256; ++u) {
+    const int q = tid + 256 * u;
+    const int row = q / (64 / VPT), c = (q % (64 / VPT)) * VPT;
+    u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
+    if (t0 + row < tokens)
+      v = *reinterpret_cast<const u32x4_t*>(H + (int64_t)(t0 + row) * D + d0 + c);
+    const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+    for (int x = 0; x < VPT; ++x) tile[row][c + x] = e[x];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 64 * 64 / VPT / 256; ++u) {
+    const int q = tid + 256 * u;
+    const int d = q / (64 / VPT), c = (q % (64 / VPT)) * VPT;
+    u32x4_t v;
+    T* e = reinterpret_cast<T*>(&v);
+#pragma unroll
+    for (int x = 0; x < VPT; ++x) e[x] = tile[c + x][d];
+    *reinterpret_cast<u32x4_t*>(Ht + (int64_t)(d0 + d) * ldt + t0 + c) = v;
+  }
+}
+
+// grad_W[v, d] (+)= sum_t dZ[t, v] H[t, d] over the tokens of a group of
+// chunks, computed as the tile C[d, v] = Ht[d, :] dZ[:, v]: A = the transposed
+// hidden rows (K = tokens contiguous, zero past the group), B = dZ read
+// K-major (rows = tokens; rows past the group read as zeros). Lane (g, c) of
+// a wave holds C at four consecutive d of one v for each block, i.e. 16
+// contiguous bytes of a grad_W row, so the tile goes to memory straight from
+// the accumulators: with beta = 1 one half of the tile's old values is loaded,
+// added, and the other half's loads are issued before the first half's stores
+// (loads and stores complete in issue order, so waiting for those loads does
+// not wait for the stores).
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ Ht, int ldt,
+                                                    const T* __restrict__ dZ, int64_t ldz,
+                                                    int tokens, int V, int D, int TM, int TN,
+                                                    int beta, float* __restrict__ gW) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
-  const int m0 = mt * kTile, n0 = nt * kTile;
+  const int m0 = mt * kTile, n0 = nt * kTile;  // m: feature d, n: vocabulary v
   const int eb = Elt<T>::bytes;
-  const int lda = (int)(ldz * eb), ldb = D * eb;
-  const int mrows = min(kTile, V - m0);
+  const int lda = ldt * eb, ldb = (int)(ldz * eb);
+  const int mrows = min(kTile, D - m0);
   constexpr int KS = kRowB / (int)sizeof(T);
   AccTile acc;
-  gemm_tile<T, KmOp, KmOp, 8, false, 3>(
-      KmOp{reinterpret_cast<const char*>(dZ + m0), (int64_t)tokens * lda - (int64_t)m0 * eb, lda},
-               KmOp{reinterpret_cast<const char*>(Hg + n0), (int64_t)tokens * ldb - (int64_t)n0 * eb, ldb},
-               0, (tokens + KS - 1) / KS, lds, acc);
-  // Output tile in two halves of 128 rows: the waves holding a half stage it
-  // in LDS (fp32, 16-float column groups XOR-swizzled by row so the staging
-  // writes of a wave's 4 row groups hit distinct banks), then every thread
-  // moves 16-byte row pieces: with beta = 1 all of its old values are loaded
-  // before any store of the half, then added and stored. Rows past V and
-  // columns past D are skipped.
+  gemm_tile<T, KcOp, KmOp, 8, true, 3>(
+      KcOp{reinterpret_cast<const char*>(Ht + (int64_t)m0 * ldt), (uint32_t)(mrows * lda), lda},
+      KmOp{reinterpret_cast<const char*>(dZ + n0), (int64_t)tokens * ldb - (int64_t)n0 * eb, ldb},
+      0, ldt / KS, lds, acc);
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
-  const int tid = threadIdx.x;
-  float* stg = reinterpret_cast<float*>(lds);  // [128][256]
-  const int ncols = min(kTile, D - n0);
+  // the tile's rows of grad_W as one resource: rows past V are out of range
+  // (loads give 0, stores are dropped), features past D get an out-of-range
+  // offset
+  const int vrows = __builtin_amdgcn_readfirstlane(min(kTile, V - n0));
+  const __amdgpu_buffer_rsrc_t ro =
+      make_rsrc(gW + (int64_t)n0 * D, (uint32_t)vrows * (uint32_t)D * 4u);
+  // block (i, j) sits at byte offset obase + 64 i (16 features) + 64 D j (16
+  // rows): the per-lane part is one register, 64 i goes into the
+  // instruction's immediate offset and 64 D j into its scalar offset. D is a
+  // multiple of 64, so whether block i's features exist is the same for the
+  // whole wave.
+  const int dw0 = m0 + wm * 128;
+  const uint32_t obase =
+      ((uint32_t)acc_n(wn, 0, lane) * (uint32_t)D + (uint32_t)(dw0 + 4 * (lane >> 4))) * 4u;
+  const uint32_t jstep = 64u * (uint32_t)D;
+  auto ld = [&](int i, int j) {
+    return __builtin_bit_cast(
+        f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ro, obase + 64u * i, jstep * j, 0));
+  };
+  auto st = [&](int i, int j, f32x4_t v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), ro, obase + 64u * i,
+                                           jstep * j, 0);
+  };
+  auto live = [&](int i) { return dw0 + 16 * i < D; };
+  if (beta) {
+    f32x4_t old[4][4];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    if (wm == h) {
+    for (int i = 0; i < 4; ++i)
+      if (live(i))
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+        for (int j = 0; j < 4; ++j) old[i][j] = ld(i, j);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+    for (int i = 0; i < 4; ++i)
+      if (live(i))
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = acc_m(0, i, lane, r);
-            const int col = acc_n(wn, j, lane) ^ (((row >> 2) & 3) << 4);
-            stg[row * 256 + col] = acc.v[i][j][r];
-          }
-    }
-    __syncthreads();
-    // rows of this half as one buffer resource: rows past V are out of
-    // range, columns past D get an out-of-range offset (loads give 0, stores
-    // are dropped), so no lane branches and no load waits behind a store
-    const int hrows = __builtin_amdgcn_readfirstlane(max(0, min(128, mrows - 128 * h)));
-    const __amdgpu_buffer_rsrc_t ro =
-        make_rsrc(gW + (int64_t)(m0 + 128 * h) * D, (uint32_t)hrows * (uint32_t)D * 4u);
-    uint32_t off[16];
+        for (int j = 0; j < 4; ++j) acc.v[i][j] += old[i][j];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int q = tid + kThreads * u;
-      const int row = q >> 6, c4 = (q & 63) * 4;
-      off[u] = c4 < ncols ? ((uint32_t)row * (uint32_t)D + (uint32_t)(n0 + c4)) * 4u : kOobOffset;
-    }
-    u32x4_t old[16];
-    if (beta) {
+    for (int i = 0; i < 4; ++i)
+      if (live(4 + i))
 #pragma unroll
-      for (int u = 0; u < 16; ++u) old[u] = __builtin_amdgcn_raw_buffer_load_b128(ro, off[u], 0, 0);
-    } else {
+        for (int j = 0; j < 4; ++j) old[i][j] = ld(4 + i, j);
 #pragma unroll
-      for (int u = 0; u < 16; ++u) old[u] = u32x4_t{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < 4; ++i)
+      if (live(i))
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int q = tid + kThreads * u;
-      const int row = q >> 6, c4 = (q & 63) * 4;
-      const f32x4_t v = *reinterpret_cast<const f32x4_t*>(stg + row * 256 + (c4 ^ (((row >> 2) & 3) << 4)));
-      const f32x4_t o = __builtin_bit_cast(f32x4_t, old[u]);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, o + v), ro, off[u], 0, 0);
-    }
-    __syncthreads();
+        for (int j = 0; j < 4; ++j) st(i, j, acc.v[i][j]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (live(4 + i))
+#pragma unroll
+        for (int j = 0; j < 4; ++j) st(4 + i, j, acc.v[4 + i][j] + old[i][j]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (live(i))
+#pragma unroll
+        for (int j = 0; j < 4; ++j) st(i, j, acc.v[i][j]);
   }
 }
 
@@ -788,11 +834,11 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 namespace {
 enum ProfKind {
   P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
-  P_DW, P_FINALIZE, P_FILL, P_NKINDS
+  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
     "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
-    "dh", "dh_reduce", "dw", "finalize_loss", "fill"};
+    "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -953,11 +999,18 @@ extern "C" int kd_launch_chunk(const KdChunkArgs* a, void* stream) {
 
 template <typename T>
 static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
-  const int TM = cdiv(a.V, kTile), TN = cdiv(a.D, kTile);
+  const int ldt = (int)(((a.tokens + 63) / 64) * 64);
+  T* Ht = static_cast<T*>(a.Ht);
+  {
+    ProfScope ps_(P_TRANSPOSE, 0.0, s);
+    hipLaunchKernelGGL(k_transpose_rows<T>, dim3(ldt / 64, (int)(a.D / 64)), dim3(256), 0, s,
+                       static_cast<const T*>(a.Hg), (int)a.tokens, (int)a.D, Ht, ldt);
+  }
+  const int TM = cdiv(a.D, kTile), TN = cdiv(a.V, kTile);
   ProfScope ps_(P_DW, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
-  hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s, static_cast<const T*>(a.dZ),
-                     a.ldz, static_cast<const T*>(a.Hg), (int)a.tokens, (int)a.V, (int)a.D, TM, TN,
-                     a.beta, a.gW);
+  hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s, static_cast<const T*>(Ht), ldt,
+                     static_cast<const T*>(a.dZ), a.ldz, (int)a.tokens, (int)a.V, (int)a.D, TM,
+                     TN, a.beta, a.gW);
   return (int)hipGetLastError();
 }
 

@@ -62,6 +62,7 @@ struct KdDwArgs {
   int64_t ldz;
   const void* Hg;           // the group's hidden rows [tokens, D]
   int64_t tokens;           // tokens in the group
+  void* Ht;                 // workspace for Hg transposed: [D, tokens rounded up to 64]
   int beta;                 // 0 overwrite, 1 accumulate
   float* gW;
 };
