@@ -596,6 +596,31 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
+// Sum / max over each row of 16 lanes, result in all 16 lanes, by DPP lane
+// moves: swap neighbours (quad_perm 1,0,3,2), swap pairs (quad_perm 2,3,0,1),
+// mirror within 8 (row_half_mirror), mirror within 16 (row_mirror).
+__device__ __forceinline__ float dpp_f(float x, int ctrl_id) {
+  const int v = __builtin_bit_cast(int, x);
+  int r;
+  switch (ctrl_id) {
+    case 0: r = __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false); break;
+    case 1: r = __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false); break;
+    case 2: r = __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false); break;
+    default: r = __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false); break;
+  }
+  return __builtin_bit_cast(float, r);
+}
+__device__ __forceinline__ float row16_sum(float x) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) x += dpp_f(x, c);
+  return x;
+}
+__device__ __forceinline__ float row16_max(float x) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) x = fmaxf(x, dpp_f(x, c));
+  return x;
+}
+
 // inclusive prefix sum over the 64 lanes of a wave
 __device__ __forceinline__ int wave_incl_scan(int x) {
   const int lane = threadIdx.x & 63;

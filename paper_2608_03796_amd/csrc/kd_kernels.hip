@@ -563,6 +563,175 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
   }
 }
 
+// ------------------------------------ one projection per chunk (fused call) --
+// A call that wants the loss and its gradients together has each chunk's
+// normaliser complete as soon as that chunk's projection has run, so the
+// chunk is projected once instead of once for log Z and again for dZ: the
+// tile records per token the max m of y = z log2(e) / tau over its columns
+// and the sum of 2^(y - m) (the same partials as k_logits_lse), z at its
+// teacher entries, and the provisional gradient dZ'' = 2^(y - m) in the dZ
+// buffer (0 past V). Once log Z is merged, k_dz_rescale scales each
+// (token, vocabulary tile) run of dZ'' by (g/tau) M 2^(m - log2 Z), which makes
+// it (g/tau) M q, and k_dz_teacher rewrites the teacher cells as
+// (g/tau)(M q - p) (Eq. 3) from the recorded z. The [c, V] buffer is the
+// same transient chunk the recompute schedule holds; nothing grows with N.
+// Staging and teacher bookkeeping are those of k_dz.
+template <typename T>
+__global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
+    const T* __restrict__ W, const T* __restrict__ Hc, int D, int V, int rows, int TM, int TN,
+    float k2, float* __restrict__ part_m, float* __restrict__ part_s, int nVT,
+    const uint32_t* __restrict__ hits, const int* __restrict__ hoff, int K, T* dZ, int64_t ldz,
+    float* zhit) {
+  __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
+  int mt, nt;
+  tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
+  const int m0 = mt * kTile, n0 = nt * kTile;
+  const int eb = Elt<T>::bytes;
+  const int ld = D * eb;
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wm = wave >> 2, wn = wave & 3;
+
+  const int64_t seg = (int64_t)nt * kTile * K;
+  const int* ho = hoff + (int64_t)nt * (nVT + 1) + mt;
+  const int hb = ho[0], cnt = ho[1] - hb;
+  const uint32_t fe = tid < cnt ? hits[seg + hb + tid] : 0u;
+
+  AccTile acc;
+  gemm_tile<T, KcOp, KcOp, 8, false, 3>(
+      KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
+      KcOp{reinterpret_cast<const char*>(Hc + (int64_t)n0 * D), (uint32_t)(nrows * ld), ld}, 0,
+      ld / kRowB, lds, acc);
+  const bool full = m0 + kTile <= V;
+
+  float* st = reinterpret_cast<float*>(lds);
+  const int rho = lane >> 4, lam = lane & 15;  // row pass: 4 token rows per wave, 16 lanes each
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if ((wn >> 1) == h) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = (wn & 1) * 64 + 16 * j + (lane & 15);  // token row of the half
+          const int vl = acc_m(wm, i, lane, 0);                 // 4 consecutive vocab
+          const int slot = (vl >> 2) ^ hsw16(n);
+          *reinterpret_cast<f32x4_t*>(st + n * 256 + slot * 4) = acc.v[i][j];
+        }
+    }
+    __syncthreads();
+    // z at the teacher entries of this half, for C = sum_k p z (Eq. 2)
+    auto rec = [&](uint32_t e) {
+      const int tl = (int)(e & 255u);
+      if ((tl >> 7) != h) return;
+      const int n = tl & 127, v = (int)((e >> 8) & 255u);
+      zhit[(int64_t)(n0 + tl) * K + (e >> 16)] =
+          st[n * 256 + ((((v >> 2) ^ hsw16(n)) << 2) | (v & 3))];
+    };
+    if (tid < cnt) rec(fe);
+    for (int q = kThreads + tid; q < cnt; q += kThreads) rec(hits[seg + hb + q]);
+
+    // 16 lanes per token row, lane lam holding columns 4 lam + 64 k + (0..3):
+    // the row's max m (in base-2 units) and sum of 2^(y - m) reduce within the
+    // 16 lanes (DPP), and 2^(y - m) goes to dZ'' as 128-byte row runs per
+    // store; columns past V give 0 and count for neither
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int n = wave * 16 + 4 * gq + rho;  // token row of the half
+      f32x4_t zr[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        zr[k] = *reinterpret_cast<const f32x4_t*>(st + n * 256 + (((lam + 16 * k) ^ hsw16(n)) << 2));
+      float mx = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (full || m0 + 4 * lam + 64 * k + e < V) mx = fmaxf(mx, zr[k][e]);
+      const float m = row16_max(mx) * k2;
+      float sum = 0.f;
+      f32x4_t G[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float ev = fast_exp2(zr[k][e] * k2 - m);
+          if (!full && m0 + 4 * lam + 64 * k + e >= V) ev = 0.f;
+          G[k][e] = ev;
+          sum += ev;
+        }
+      sum = row16_sum(sum);
+      const int t = n0 + 128 * h + n;
+      if (t < rows) {
+        T* dst = dZ + (int64_t)t * ldz + m0 + 4 * lam;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if constexpr (sizeof(T) == 2) {
+            const u32x2_t pk2 = {pack_bf16x2(G[k][0], G[k][1]), pack_bf16x2(G[k][2], G[k][3])};
+            *reinterpret_cast<u32x2_t*>(dst + 64 * k) = pk2;
+          } else {
+            *reinterpret_cast<f32x4_t*>(dst + 64 * k) = G[k];
+          }
+        }
+        if (lam == 0) {
+          part_m[(int64_t)t * nVT + mt] = m;
+          part_s[(int64_t)t * nVT + mt] = sum;
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// dZ[t, v] = (g/tau)_t M_t 2^(m_tb - log2 Z_t) dZ''[t, v] with b = v / 256:
+// one 16-byte run of a row per thread; grid (rows, column blocks).
+template <typename T>
+__global__ __launch_bounds__(256) void k_dz_rescale(T* __restrict__ dZ, int64_t ldz, int nVT,
+                                                    const float* __restrict__ part_m,
+                                                    const float* __restrict__ rowL2,
+                                                    const float* __restrict__ rowCoefM) {
+  constexpr int VPT = 16 / (int)sizeof(T);
+  const int t = blockIdx.x;
+  const int64_t c0 = ((int64_t)blockIdx.y * 256 + threadIdx.x) * VPT;
+  if (c0 >= ldz) return;
+  const float f = rowCoefM[t] * fast_exp2(part_m[(int64_t)t * nVT + (c0 >> 8)] - rowL2[t]);
+  // the result is built as a new vector (element-wise updates of a vector in
+  // place were miscompiled: later elements were computed from updated ones)
+  u32x4_t* q = reinterpret_cast<u32x4_t*>(dZ + (int64_t)t * ldz + c0);
+  const u32x4_t v = *q;
+  if constexpr (sizeof(T) == 2) {
+    uint32_t o[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t x = v[w];
+      o[w] = pack_bf16x2(__builtin_bit_cast(float, x << 16) * f,
+                         __builtin_bit_cast(float, x & 0xffff0000u) * f);
+    }
+    *q = u32x4_t{o[0], o[1], o[2], o[3]};
+  } else {
+    *q = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) * f);
+  }
+}
+
+// The teacher cells of dZ: (g/tau) M 2^(z log2(e)/tau - log2 Z) - (g/tau) p, one
+// thread per entry of the chunk (indices outside [0, V) are skipped).
+template <typename T>
+__global__ __launch_bounds__(256) void k_dz_teacher(T* __restrict__ dZ, int64_t ldz,
+                                                    const int32_t* __restrict__ tidx,
+                                                    const float* __restrict__ p,
+                                                    const float* __restrict__ zhit, int rows,
+                                                    int K, int V, float k2,
+                                                    const float* __restrict__ rowL2,
+                                                    const float* __restrict__ rowCoef,
+                                                    const float* __restrict__ rowCoefM) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)rows * K) return;
+  const int v = tidx[e];
+  if ((unsigned)v >= (unsigned)V) return;
+  const int t = (int)(e / K);
+  dZ[(int64_t)t * ldz + v] = (T)(rowCoefM[t] * fast_exp2(zhit[e] * k2 - rowL2[t]) - rowCoef[t] * p[e]);
+}
+
 // l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2) with C_t = sum_k p_k z_{t, idx_k},
 // 0 on ignored rows; per-block partial sums in a fixed order for the
 // deterministic mean.
@@ -693,7 +862,8 @@ __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H,
     u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
     if (t0 + row < tokens)
       v = *reinterpret_cast<const u32x4_t*>(H + (int64_t)(t0 + row) * D + d0 + c);
-    const T* e = reinterpret_cast<const T*>(&v);
+    T e[VPT];
+    __builtin_memcpy(e, &v, 16);
 #pragma unroll
     for (int x = 0; x < VPT; ++x) tile[row][c + x] = e[x];
   }
@@ -702,10 +872,11 @@ __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H,
   for (int u = 0; u < 64 * 64 / VPT / 256; ++u) {
     const int q = tid + 256 * u;
     const int d = q / (64 / VPT), c = (q % (64 / VPT)) * VPT;
-    u32x4_t v;
-    T* e = reinterpret_cast<T*>(&v);
+    T e[VPT];
 #pragma unroll
     for (int x = 0; x < VPT; ++x) e[x] = tile[c + x][d];
+    u32x4_t v;
+    __builtin_memcpy(&v, e, 16);
     *reinterpret_cast<u32x4_t*>(Ht + (int64_t)(d0 + d) * ldt + t0 + c) = v;
   }
 }
@@ -834,11 +1005,12 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 namespace {
 enum ProfKind {
   P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
-  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_NKINDS
+  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_RESCALE, P_DZ_TEACHER, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
     "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
-    "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows"};
+    "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows", "logits_dz", "dz_rescale",
+    "dz_teacher"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -942,28 +1114,58 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(k_bucket, dim3(TNt), dim3(kBucketThreads), 0, s, a.tidx, a.p, a.rows, a.K,
                        (int)a.V, a.nVT, a.hits, a.hitp, a.hoff, a.zhit);
     }
-  if (fwd) {
+  if (fwd && bwd && a.dZ != nullptr) {
+    // loss and gradients together: one projection per chunk (k_logits_dz),
+    // then the merge of log Z, the rescale of the provisional dZ and its
+    // teacher cells
     {
-      ProfScope ps_(P_LOGITS, gemm_flops, s);
-      // forward-only: z at the teacher entries comes from this GEMM, and
-      // there is no logit recompute
-      hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
+      ProfScope ps_(P_LOGITS_DZ, gemm_flops, s);
+      hipLaunchKernelGGL(k_logits_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
                          (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT, a.hits,
-                         a.hoff, a.K, bwd ? nullptr : a.zhit);
+                         a.hoff, a.K, static_cast<T*>(a.dZ), a.ldz, a.zhit);
     }
     {
       ProfScope ps_(P_MERGE, 0.0, s);
       hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
                          a.rows, a.nVT, a.rowL2);
     }
-  }
-  if (bwd) {
-    // z at the teacher entries is recorded here in the fused call (the
-    // backward-only call has no use for it)
-    ProfScope ps_(P_DZ, gemm_flops, s);
-    hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D, (int)a.V,
-                       a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits, a.hitp,
-                       a.hoff, a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz, fwd ? a.zhit : nullptr);
+    {
+      ProfScope ps_(P_RESCALE, 0.0, s);
+      const int cb = cdiv(a.ldz, 256 * (16 / (int)sizeof(T)));
+      hipLaunchKernelGGL(k_dz_rescale<T>, dim3(a.rows, cb), dim3(256), 0, s,
+                         static_cast<T*>(a.dZ), a.ldz, a.nVT, a.part_m, a.rowL2, a.rowCoefM);
+    }
+    {
+      ProfScope ps_(P_DZ_TEACHER, 0.0, s);
+      hipLaunchKernelGGL(k_dz_teacher<T>, dim3(cdiv((int64_t)a.rows * a.K, 256)), dim3(256), 0, s,
+                         static_cast<T*>(a.dZ), a.ldz, a.tidx, a.p, a.zhit, a.rows, a.K, (int)a.V,
+                         k2, a.rowL2, a.rowCoef, a.rowCoefM);
+    }
+  } else {
+    if (fwd) {
+      {
+        ProfScope ps_(P_LOGITS, gemm_flops, s);
+        // no recompute follows (forward only, or a fused call that wants no
+        // gradients): z at the teacher entries comes from this GEMM
+        hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc,
+                           (int)a.D, (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT,
+                           a.hits, a.hoff, a.K, a.zhit);
+      }
+      {
+        ProfScope ps_(P_MERGE, 0.0, s);
+        hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m,
+                           a.part_s, a.rows, a.nVT, a.rowL2);
+      }
+    }
+    if (bwd && !fwd) {
+      // the backward of the split entry points: the logit recompute from the
+      // saved log Z (Algorithm 1's backward)
+      ProfScope ps_(P_DZ, gemm_flops, s);
+      hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
+                         (int)a.V, a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits,
+                         a.hitp, a.hoff, a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz,
+                         (float*)nullptr);
+    }
   }
   if (fwd) {
     ProfScope ps_(P_ROW_LOSS, 0.0, s);
