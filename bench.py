@@ -2,9 +2,12 @@
 """Throughput of the fused chunked top-K KL loss (forward + backward) on one MI355X.
 
 One step = one kd_topk_kl_fwd_bwd call over the whole workload: teacher
-prologue, the chunked logits / online log-normaliser, the logit recompute with
-the closed-form gradient, and the dH and dW contractions, for every chunk.
-Inputs are synthetic (seeded) and resident in HBM before the timed region.
+prologue, then for every chunk the projection with the online log-normaliser
+and the provisional gradient, the normaliser merge, the gradient rescale with
+the teacher correction (Eq. 3), and the dH and dW contractions. The same step
+through the split entry points (forward, then a backward that recomputes the
+logits, as Algorithm 1 does) is timed beside it. Inputs are synthetic (seeded)
+and resident in HBM before the timed region.
 
 Prints one JSON line. `roofline` is for the kernel with the largest total time,
 from HIP events the library records around each of its launches during the

@@ -123,6 +123,14 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  *                                     16-byte aligned
  *   hip_stream                        hipStream_t or NULL
  *
+ * Schedule: with grad_hidden or grad_W requested, each chunk is projected
+ * once. A chunk's log Z is complete once its own projection has run, and the
+ * upstream gradient of the mean is known up front, so the projection that
+ * yields the normaliser also yields the gradient, with one rescale per
+ * (token, vocabulary tile) after the merge of log Z, in place of Algorithm
+ * 1's logit recompute (which the split entry points below keep). The
+ * transient [chunk, V] buffer is the same one; nothing of size N x V exists.
+ *
  * Pointers hidden, W, grad_hidden, grad_W and workspace must be 16-byte
  * aligned (KD_ERR_UNSUPPORTED otherwise). hidden, W, teacher_idx,
  * teacher_logit and loss are required (KD_ERR_NULL_PTR); with N == 0 only
