@@ -80,6 +80,27 @@ def test_backward_matches_oracle(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N,D,V,K,chunk,tau,ign", SHAPES + [(600, 128, 777, 5, 128, 0.5, 0.1)])
+def test_fused_schedule_matches_split(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
+    """The fused call projects each chunk once and rescales a provisional dZ;
+    the split entry points recompute the logits (Algorithm 1). Same loss up to
+    the order of the normaliser's fp32 sums; gradients within the fused path's
+    second bf16 rounding of dZ (2^-8 relative), or fp32 rounding."""
+    kd = gpu_lib
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=N + 5, ignore_frac=ign)
+    fb = kd.fwd_bwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True)
+    f = kd.fwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True)
+    b = kd.bwd(*_args(inp), f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk)
+    torch.cuda.synchronize()
+    assert abs(float(fb["loss"]) - float(f["loss"])) <= 1e-6 * abs(float(f["loss"]))
+    assert rel_max(to64(fb["loss_per_token"]), to64(f["loss_per_token"])) <= 1e-6
+    gt = 1e-6 if dtype == "f32" else 2.0 ** -7
+    assert rel_max(to64(fb["grad_hidden"]), to64(b["grad_hidden"])) <= gt
+    assert rel_max(to64(fb["grad_W"]), to64(b["grad_W"])) <= gt
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_upstream_scalar_and_per_token(gpu_lib, dtype):
     kd = gpu_lib
     N, D, V, K, chunk, tau = 259, 128, 4133, 7, 100, 2.0
