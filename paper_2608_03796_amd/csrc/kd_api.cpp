@@ -34,8 +34,10 @@ struct Plan {
   int64_t nVT;         // vocabulary tiles
   int64_t nchunks;
   int64_t nblk;        // loss partials of a full chunk (one per 16 rows)
-  int64_t G;           // chunks whose dZ rows are gathered before one dW GEMM
-  int dh_split;
+  int64_t G;           // chunks whose dZ rows are gathered before one dH and one dW GEMM
+  int64_t ngroups;
+  bool dh_per_group;   // dH once per group (a chunk alone has too few tiles) or per chunk
+  int64_t td, ksteps;  // dH column tiles and K steps (for its vocabulary split)
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
       off_lossp, off_dz, off_ht, off_dhs, total;
 };
@@ -89,8 +91,21 @@ Plan make_plan(const kd_problem* p) {
   pl.G = std::max<int64_t>(1, std::min<int64_t>(16384 / pl.c, std::max<int64_t>(pl.nchunks, 1)));
   pl.G = std::max<int64_t>(
       1, std::min<int64_t>(pl.G, ((int64_t)4 << 30) / std::max<int64_t>(pl.c * pl.Vp * pl.eb, 1)));
-  const int64_t dh_tiles = cdiv(pl.c, kTile) * cdiv(pl.D, kTile);
-  pl.dh_split = choose_dh_split(dh_tiles, pl.Vp * pl.eb / 128);
+  // dH runs per chunk when a chunk's tiles fill the chip, else once per group
+  // of G chunks (G times the tiles, dW's grouping); its vocabulary range is
+  // split only when the rows it covers still have too few tiles
+  pl.ngroups = cdiv(pl.nchunks, pl.G);
+  pl.td = cdiv(pl.D, kTile);
+  pl.ksteps = pl.Vp * pl.eb / 128;
+  pl.dh_per_group = choose_dh_split(cdiv(pl.c, kTile) * pl.td, pl.ksteps) > 1;
+  int64_t dh_rows[2];  // the row counts dH runs on: full and last chunk or group
+  if (pl.dh_per_group) {
+    dh_rows[0] = std::min<int64_t>(pl.G * pl.c, pl.N);
+    dh_rows[1] = pl.N - (pl.ngroups - 1) * pl.G * pl.c;
+  } else {
+    dh_rows[0] = pl.c;
+    dh_rows[1] = pl.N - (pl.nchunks - 1) * pl.c;
+  }
   size_t t = 0;
   auto take = [&](size_t bytes) {
     const size_t o = align256(t);
@@ -110,7 +125,15 @@ Plan make_plan(const kd_problem* p) {
   pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
   // the hidden rows of one dW group, transposed (tokens padded to 64)
   pl.off_ht = take((size_t)pl.D * rup(pl.G * pl.c, 64) * pl.eb);
-  pl.off_dhs = pl.dh_split > 1 ? take((size_t)pl.dh_split * pl.c * pl.D * 4) : 0;
+  {
+    int64_t part = 0;
+    for (int64_t r : dh_rows) {
+      if (r <= 0) continue;
+      const int sp = choose_dh_split(cdiv(r, kTile) * pl.td, pl.ksteps);
+      if (sp > 1) part = std::max<int64_t>(part, sp * r);
+    }
+    pl.off_dhs = part > 0 ? take((size_t)part * pl.D * 4) : 0;
+  }
   pl.total = align256(t);
   return pl;
 }
@@ -249,30 +272,47 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     const int64_t slot = ci % pl.G;
     a.dZ = (want_dh || want_dw) ? ws + pl.off_dz + slot * pl.c * pl.Vp * pl.eb : nullptr;
     a.ldz = pl.Vp;
-    a.dh_split = pl.dh_split;
-    a.dh_partial = pl.dh_split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
     a.loss_per_token = c.lpt ? c.lpt + row0 : nullptr;
     a.block_partial = lossp + n_partials;
-    a.gH = want_dh ? static_cast<char*>(c.grad_hidden) + row0 * pl.D * pl.eb : nullptr;
     if (kd_launch_chunk(&a, c.stream) != 0) return KD_ERR_DEVICE;
     n_partials += cdiv(rcount, 16);
     group_tokens += rcount;
-    if (want_dw && (slot == pl.G - 1 || ci == pl.nchunks - 1)) {
+    // dH over rows [r0, r0 + n) of the dZ buffer (from its row `zrow`)
+    auto dh = [&](int64_t r0, int64_t n, int64_t zrow) -> bool {
+      KdDhArgs h{};
+      h.dtype = p->dtype;
+      h.D = pl.D;
+      h.V = pl.V;
+      h.dZ = ws + pl.off_dz + zrow * pl.Vp * pl.eb;
+      h.ldz = pl.Vp;
+      h.W = c.W;
+      h.tokens = n;
+      h.split = choose_dh_split(cdiv(n, kTile) * pl.td, pl.ksteps);
+      h.partial = h.split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
+      h.gH = static_cast<char*>(c.grad_hidden) + r0 * pl.D * pl.eb;
+      return kd_launch_dh(&h, c.stream) == 0;
+    };
+    if (want_dh && !pl.dh_per_group && !dh(row0, rcount, slot * pl.c)) return KD_ERR_DEVICE;
+    if (!(want_dh || want_dw) || !(slot == pl.G - 1 || ci == pl.nchunks - 1)) continue;
+    // the group's dH (when it runs per group) and dW over the G chunks' dZ rows
+    const int64_t row_first = row0 + rcount - group_tokens;
+    if (want_dh && pl.dh_per_group && !dh(row_first, group_tokens, 0)) return KD_ERR_DEVICE;
+    if (want_dw) {
       KdDwArgs d{};
       d.dtype = p->dtype;
       d.D = pl.D;
       d.V = pl.V;
       d.dZ = ws + pl.off_dz;
       d.ldz = pl.Vp;
-      d.Hg = static_cast<const char*>(c.hidden) + (row0 + rcount - group_tokens) * pl.D * pl.eb;
+      d.Hg = static_cast<const char*>(c.hidden) + row_first * pl.D * pl.eb;
       d.tokens = group_tokens;
       d.Ht = ws + pl.off_ht;
       d.beta = (dw_done || c.accumulate) ? 1 : 0;
       d.gW = c.grad_W;
       if (kd_launch_dw(&d, c.stream) != 0) return KD_ERR_DEVICE;
       dw_done = true;
-      group_tokens = 0;
     }
+    group_tokens = 0;
   }
   if (fwd && kd_launch_finalize(lossp, (int)n_partials, inv_nvalid, c.loss, c.stream) != 0)
     return KD_ERR_DEVICE;

@@ -1173,30 +1173,37 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                        a.K, a.rowL2, a.rowM, a.rowH, a.ignore, a.row0, a.rows, a.inv_tau,
                        a.loss_per_token, a.logz_out, a.block_partial);
   }
-  if (bwd && a.gH != nullptr) {
-    const int TM = cdiv(a.rows, kTile), TN = cdiv(a.D, kTile);
-    const int ks = (int)(a.ldz * sizeof(T) / kRowB);
-{
-    ProfScope ps_(P_DH, gemm_flops, s);
-    hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.dh_split), dim3(kThreads), 0, s,
-                       static_cast<const T*>(a.dZ), a.ldz, W, (int)a.V, a.rows, (int)a.D, TM, TN,
-                       ks, a.dh_split, static_cast<T*>(a.gH), a.dh_partial);
-    }
-    if (a.dh_split > 1) {
-      const int64_t n = (int64_t)a.rows * a.D;
-{
-    ProfScope ps_(P_DH_REDUCE, 0.0, s);
-    hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256),
-                         0, s, a.dh_partial, a.dh_split, n, static_cast<T*>(a.gH));
-    }
-    }
-  }
   return (int)hipGetLastError();
 }
 
 extern "C" int kd_launch_chunk(const KdChunkArgs* a, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   return a->dtype == 1 ? launch_chunk_impl<__bf16>(*a, s) : launch_chunk_impl<float>(*a, s);
+}
+
+template <typename T>
+static int launch_dh_impl(const KdDhArgs& a, hipStream_t s) {
+  const int rows = (int)a.tokens;
+  const int TM = cdiv(rows, kTile), TN = cdiv(a.D, kTile);
+  const int ks = (int)(a.ldz * sizeof(T) / kRowB);
+  {
+    ProfScope ps_(P_DH, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
+    hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.split), dim3(kThreads), 0, s,
+                       static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.W), (int)a.V,
+                       rows, (int)a.D, TM, TN, ks, a.split, static_cast<T*>(a.gH), a.partial);
+  }
+  if (a.split > 1) {
+    const int64_t n = (int64_t)rows * a.D;
+    ProfScope ps_(P_DH_REDUCE, 0.0, s);
+    hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256), 0,
+                       s, a.partial, a.split, n, static_cast<T*>(a.gH));
+  }
+  return (int)hipGetLastError();
+}
+
+extern "C" int kd_launch_dh(const KdDhArgs* a, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return a->dtype == 1 ? launch_dh_impl<__bf16>(*a, s) : launch_dh_impl<float>(*a, s);
 }
 
 template <typename T>

@@ -46,12 +46,22 @@ struct KdChunkArgs {
   float* zhit;              // [rows, K] student logit at each teacher entry
   void* dZ;                 // this chunk's rows of the group's dZ [rows, ldz]
   int64_t ldz;              // = padded vocabulary (columns V..ldz: finite, z = 0 there)
-  int dh_split;
-  float* dh_partial;        // [dh_split, rows, D] when dh_split > 1
   // outputs
   float* loss_per_token;    // + row0, or null
   float* block_partial;     // this chunk's cdiv(rows, 16) partial sums
-  void* gH;                 // grad_hidden + row0 * D, or null
+};
+
+// dH GEMM over the chunks of one group: grad_hidden[rows] = dZ[rows] W
+struct KdDhArgs {
+  int dtype;
+  int64_t D, V;
+  const void* dZ;           // the group's dZ rows [tokens, ldz]
+  int64_t ldz;
+  const void* W;            // [V, D]
+  int64_t tokens;           // tokens in the group
+  int split;                // split of the vocabulary (K) range, >= 1
+  float* partial;           // [split, tokens, D] when split > 1
+  void* gH;                 // grad_hidden + the group's first row * D
 };
 
 // dW GEMM over the chunks of one group: grad_W (+)= dZ[:tokens]^T H[:tokens]
@@ -70,6 +80,7 @@ struct KdDwArgs {
 extern "C" {
 int kd_launch_prepare(const KdPrepareArgs* a, void* stream);
 int kd_launch_chunk(const KdChunkArgs* a, void* stream);
+int kd_launch_dh(const KdDhArgs* a, void* stream);
 int kd_launch_dw(const KdDwArgs* a, void* stream);
 int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid, float* loss,
                        void* stream);
