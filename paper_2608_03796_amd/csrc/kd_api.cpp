@@ -39,7 +39,7 @@ struct Plan {
   bool dh_per_group;   // dH once per group (a chunk alone has too few tiles) or per chunk
   int64_t td, ksteps;  // dH column tiles and K steps (for its vocabulary split)
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
-      off_lossp, off_dz, off_ht, off_dhs, total;
+      off_lossp, off_dz, off_fac, off_ht, off_dhs, total;
 };
 
 kd_status check_problem(const kd_problem* p) {
@@ -114,7 +114,7 @@ Plan make_plan(const kd_problem* p) {
   };
   pl.off_misc = take(256);
   pl.off_p = take((size_t)pl.cp * pl.K * 4);
-  pl.off_rows = take((size_t)6 * pl.cp * 4);
+  pl.off_rows = take((size_t)8 * pl.cp * 4);
   pl.off_pm = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_hits = take((size_t)pl.cp * pl.K * 4);
@@ -123,6 +123,8 @@ Plan make_plan(const kd_problem* p) {
   pl.off_zhit = take((size_t)pl.cp * pl.K * 4);
   pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
   pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
+  // factor of each dZ row of the group in the single-projection schedule
+  pl.off_fac = take((size_t)pl.G * pl.c * 4);
   // the hidden rows of one dW group, transposed (tokens padded to 64)
   pl.off_ht = take((size_t)pl.D * rup(pl.G * pl.c, 64) * pl.eb);
   {
@@ -230,6 +232,10 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
   if (kd_launch_prepare(&pa, c.stream) != 0) return KD_ERR_DEVICE;
 
   float* rows = reinterpret_cast<float*>(ws + pl.off_rows);
+  float* fac = reinterpret_cast<float*>(ws + pl.off_fac);
+  // the single-projection schedule stores dZ up to a factor per row, which
+  // dH applies to its rows and dW to the hidden rows
+  const bool scaled = fwd && bwd && (want_dh || want_dw);
   int64_t n_partials = 0;
   int64_t group_tokens = 0;
   bool dw_done = false;
@@ -262,6 +268,9 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.rowCoef = rows + 2 * pl.cp;
     a.rowCoefM = rows + 3 * pl.cp;
     a.rowL2 = rows + 4 * pl.cp;
+    a.rowR = rows + 5 * pl.cp;
+    a.rowMx = rows + 6 * pl.cp;
+    a.rowFlag = reinterpret_cast<int*>(rows + 7 * pl.cp);
     a.part_m = reinterpret_cast<float*>(ws + pl.off_pm);
     a.part_s = reinterpret_cast<float*>(ws + pl.off_ps);
     a.hits = reinterpret_cast<uint32_t*>(ws + pl.off_hits);
@@ -270,6 +279,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.zhit = reinterpret_cast<float*>(ws + pl.off_zhit);
     a.nVT = (int)pl.nVT;
     const int64_t slot = ci % pl.G;
+    a.rowFactor = fac + slot * pl.c;
     a.dZ = (want_dh || want_dw) ? ws + pl.off_dz + slot * pl.c * pl.Vp * pl.eb : nullptr;
     a.ldz = pl.Vp;
     a.loss_per_token = c.lpt ? c.lpt + row0 : nullptr;
@@ -290,6 +300,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       h.split = choose_dh_split(cdiv(n, kTile) * pl.td, pl.ksteps);
       h.partial = h.split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
       h.gH = static_cast<char*>(c.grad_hidden) + r0 * pl.D * pl.eb;
+      h.rowscale = scaled ? fac + zrow : nullptr;
       return kd_launch_dh(&h, c.stream) == 0;
     };
     if (want_dh && !pl.dh_per_group && !dh(row0, rcount, slot * pl.c)) return KD_ERR_DEVICE;
@@ -309,6 +320,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       d.Ht = ws + pl.off_ht;
       d.beta = (dw_done || c.accumulate) ? 1 : 0;
       d.gW = c.grad_W;
+      d.rowscale = scaled ? fac : nullptr;
       if (kd_launch_dw(&d, c.stream) != 0) return KD_ERR_DEVICE;
       dw_done = true;
     }

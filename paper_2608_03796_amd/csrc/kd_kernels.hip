@@ -275,7 +275,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
 // log2 of the normaliser per token from the vocabulary-tile partials (fixed
 // order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau).
 __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, int nVT,
-                            float* rowL2) {
+                            float* rowL2, const float* rowR, const int* rowFlag,
+                            const float* rowCoefM, float* rowMx, float* rowFactor) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
@@ -290,7 +291,18 @@ __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, 
     if (m != -INFINITY) s += ps[j] * fast_exp2(m - mx);
   }
   s = wave_sum(s);
-  if (lane == 0) rowL2[r] = mx + log2f(s);
+  if (lane == 0) {
+    const float L2 = mx + log2f(s);
+    rowL2[r] = L2;
+    if (rowFactor != nullptr) {
+      // the factor that turns the row's stored 2^(y - ref) into (g/tau) M q:
+      // ref is the token's reference logit, or its row max when a tile fell
+      // back to its own max (the row is then rescaled to the row max)
+      const float ref = rowFlag[r] ? mx : rowR[r];
+      rowMx[r] = mx;
+      rowFactor[r] = rowCoefM[r] * fast_exp2(ref - L2);
+    }
+  }
 }
 
 // ------------------------------------------------ teacher entry buckets ----
@@ -403,6 +415,9 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __rest
 // it; then one wave per token row forms G = (g/tau) M 2^(y - L2) elsewhere and
 // stores the row of dZ[rows, Vp] (columns V..Vp as zeros).
 __device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
+
+// largest exponent (base 2) of a stored provisional gradient 2^(y - R)
+constexpr float kRefGap = 40.f;
 
 // epilogue LDS (the main loop's stages are free by then): staging [0, 128 KiB)
 constexpr int kDzBits = kLdsMain;              // 128 x 256-bit hit map of one half
@@ -569,19 +584,21 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
 // chunk is projected once instead of once for log Z and again for dZ: the
 // tile records per token the max m of y = z log2(e) / tau over its columns
 // and the sum of 2^(y - m) (the same partials as k_logits_lse), z at its
-// teacher entries, and the provisional gradient dZ'' = 2^(y - m) in the dZ
-// buffer (0 past V). Once log Z is merged, k_dz_rescale scales each
-// (token, vocabulary tile) run of dZ'' by (g/tau) M 2^(m - log2 Z), which makes
-// it (g/tau) M q, and k_dz_teacher rewrites the teacher cells as
-// (g/tau)(M q - p) (Eq. 3) from the recorded z. The [c, V] buffer is the
-// same transient chunk the recompute schedule holds; nothing grows with N.
-// Staging and teacher bookkeeping are those of k_dz.
+// teacher entries, and the provisional gradient dZ'' = 2^(y - R) in the dZ
+// buffer (0 past V), R being the token's reference logit from k_ref_logit.
+// Once log Z is merged, the row factor (g/tau) M 2^(R - log2 Z) turns dZ''
+// into (g/tau) M q; it is applied to the rows of dH and, through the
+// transposed hidden rows, to dW, so dZ'' is never rewritten, except the
+// teacher cells (k_dz_teacher writes (g/tau)(M q - p) / factor, Eq. 3) and the
+// rare rows where a tile's max exceeded R by more than kRefGap (k_dz_fix).
+// The [c, V] buffer is the same transient chunk the recompute schedule holds;
+// nothing grows with N. Staging and teacher bookkeeping are those of k_dz.
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
     const T* __restrict__ W, const T* __restrict__ Hc, int D, int V, int rows, int TM, int TN,
     float k2, float* __restrict__ part_m, float* __restrict__ part_s, int nVT,
     const uint32_t* __restrict__ hits, const int* __restrict__ hoff, int K, T* dZ, int64_t ldz,
-    float* zhit) {
+    float* zhit, const float* __restrict__ rowR, int* rowFlag) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
@@ -663,19 +680,27 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
       sum = row16_sum(sum);
       const int t = n0 + 128 * h + n;
       if (t < rows) {
+        // stored against the token's reference R (dZ'' = 2^(y - R), at most
+        // 2^kRefGap), or against the tile max m when m exceeds R by more
+        // (the token is then flagged for a row rescale)
+        const float R = rowR[t];
+        const bool own = !(m - R <= kRefGap);
+        const float cmul = own ? 1.f : fast_exp2(m - R);
         T* dst = dZ + (int64_t)t * ldz + m0 + 4 * lam;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
+          const f32x4_t Gs = G[k] * cmul;
           if constexpr (sizeof(T) == 2) {
-            const u32x2_t pk2 = {pack_bf16x2(G[k][0], G[k][1]), pack_bf16x2(G[k][2], G[k][3])};
+            const u32x2_t pk2 = {pack_bf16x2(Gs[0], Gs[1]), pack_bf16x2(Gs[2], Gs[3])};
             *reinterpret_cast<u32x2_t*>(dst + 64 * k) = pk2;
           } else {
-            *reinterpret_cast<f32x4_t*>(dst + 64 * k) = G[k];
+            *reinterpret_cast<f32x4_t*>(dst + 64 * k) = Gs;
           }
         }
         if (lam == 0) {
           part_m[(int64_t)t * nVT + mt] = m;
           part_s[(int64_t)t * nVT + mt] = sum;
+          if (own) rowFlag[t] = 1;
         }
       }
     }
@@ -683,38 +708,93 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
   }
 }
 
-// dZ[t, v] = (g/tau)_t M_t 2^(m_tb - log2 Z_t) dZ''[t, v] with b = v / 256:
-// one 16-byte run of a row per thread; grid (rows, column blocks).
+// The reference logit of each token for k_logits_dz: R = z log2(e)/tau at the
+// teacher entry with the largest teacher logit (a valid index), one wave per
+// token; -inf when the row has no valid index. R never exceeds the row's max y
+// beyond rounding, so 2^(y - R) keeps every term that matters; a tile whose max
+// exceeds R by more than kRefGap falls back to its own max. Also clears the
+// row's fallback flag.
 template <typename T>
-__global__ __launch_bounds__(256) void k_dz_rescale(T* __restrict__ dZ, int64_t ldz, int nVT,
-                                                    const float* __restrict__ part_m,
-                                                    const float* __restrict__ rowL2,
-                                                    const float* __restrict__ rowCoefM) {
-  constexpr int VPT = 16 / (int)sizeof(T);
-  const int t = blockIdx.x;
-  const int64_t c0 = ((int64_t)blockIdx.y * 256 + threadIdx.x) * VPT;
-  if (c0 >= ldz) return;
-  const float f = rowCoefM[t] * fast_exp2(part_m[(int64_t)t * nVT + (c0 >> 8)] - rowL2[t]);
-  // the result is built as a new vector (element-wise updates of a vector in
-  // place were miscompiled: later elements were computed from updated ones)
-  u32x4_t* q = reinterpret_cast<u32x4_t*>(dZ + (int64_t)t * ldz + c0);
-  const u32x4_t v = *q;
-  if constexpr (sizeof(T) == 2) {
-    uint32_t o[4];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const uint32_t x = v[w];
-      o[w] = pack_bf16x2(__builtin_bit_cast(float, x << 16) * f,
-                         __builtin_bit_cast(float, x & 0xffff0000u) * f);
+__global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, int D,
+                            const int32_t* __restrict__ tidx, const float* __restrict__ tlogit,
+                            int64_t row0, int rows, int K, int V, float k2, float* rowR,
+                            int* rowFlag) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + wave_id();
+  if (r >= rows) return;
+  const int32_t* ix = tidx + (int64_t)r * K;
+  const float* tl = tlogit + (row0 + r) * (int64_t)K;
+  float best = -INFINITY;
+  int bk = K;
+  for (int k = lane; k < K; k += 64) {
+    const int v = ix[k];
+    if ((unsigned)v < (unsigned)V && (tl[k] > best || (tl[k] == best && k < bk))) {
+      best = tl[k];
+      bk = k;
     }
-    *q = u32x4_t{o[0], o[1], o[2], o[3]};
-  } else {
-    *q = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) * f);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float ob = __shfl_xor(best, o);
+    const int ok = __shfl_xor(bk, o);
+    if (ob > best || (ob == best && ok < bk)) {
+      best = ob;
+      bk = ok;
+    }
+  }
+  float z = 0.f;
+  if (bk < K) {
+    const T* h = Hc + (int64_t)r * D;
+    const T* w = W + (int64_t)ix[bk] * D;
+    for (int d = lane; d < D; d += 64) z += (float)h[d] * (float)w[d];
+    z = wave_sum(z);
+  }
+  if (lane == 0) {
+    rowR[r] = bk < K ? z * k2 : -INFINITY;
+    rowFlag[r] = 0;
   }
 }
 
-// The teacher cells of dZ: (g/tau) M 2^(z log2(e)/tau - log2 Z) - (g/tau) p, one
-// thread per entry of the chunk (indices outside [0, V) are skipped).
+// Rows whose projection fell back to a tile's own max for some tile: every
+// run of the row is brought to the row max M (2^(ref - M) <= 1 with ref the
+// run's reference), which the row's factor was formed with. One workgroup per
+// row; unflagged rows return at once.
+template <typename T>
+__global__ __launch_bounds__(256) void k_dz_fix(T* __restrict__ dZ, int64_t ldz, int nVT,
+                                                const float* __restrict__ part_m,
+                                                const float* __restrict__ rowR,
+                                                const int* __restrict__ rowFlag,
+                                                const float* __restrict__ rowMx) {
+  const int t = blockIdx.x;
+  if (rowFlag[t] == 0) return;
+  constexpr int VPT = 16 / (int)sizeof(T);
+  const float R = rowR[t], M = rowMx[t];
+  for (int64_t c0 = (int64_t)threadIdx.x * VPT; c0 < ldz; c0 += 256 * VPT) {
+    const float m = part_m[(int64_t)t * nVT + (c0 >> 8)];
+    const float ref = !(m - R <= kRefGap) ? m : R;
+    const float f = fast_exp2(ref - M);
+    u32x4_t* q = reinterpret_cast<u32x4_t*>(dZ + (int64_t)t * ldz + c0);
+    const u32x4_t v = *q;
+    // built as a new vector (in-place element updates were miscompiled)
+    if constexpr (sizeof(T) == 2) {
+      uint32_t o[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t x = v[w];
+        o[w] = pack_bf16x2(__builtin_bit_cast(float, x << 16) * f,
+                           __builtin_bit_cast(float, x & 0xffff0000u) * f);
+      }
+      *q = u32x4_t{o[0], o[1], o[2], o[3]};
+    } else {
+      *q = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) * f);
+    }
+  }
+}
+
+// The teacher cells of dZ: (g/tau) M 2^(z log2(e)/tau - log2 Z) - (g/tau) p in
+// the row's stored scale (divided by the row factor; 0 where the factor is 0,
+// i.e. on ignored rows), one thread per entry of the chunk (indices outside
+// [0, V) are skipped).
 template <typename T>
 __global__ __launch_bounds__(256) void k_dz_teacher(T* __restrict__ dZ, int64_t ldz,
                                                     const int32_t* __restrict__ tidx,
@@ -723,13 +803,16 @@ __global__ __launch_bounds__(256) void k_dz_teacher(T* __restrict__ dZ, int64_t 
                                                     int K, int V, float k2,
                                                     const float* __restrict__ rowL2,
                                                     const float* __restrict__ rowCoef,
-                                                    const float* __restrict__ rowCoefM) {
+                                                    const float* __restrict__ rowCoefM,
+                                                    const float* __restrict__ rowFactor) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (e >= (int64_t)rows * K) return;
   const int v = tidx[e];
   if ((unsigned)v >= (unsigned)V) return;
   const int t = (int)(e / K);
-  dZ[(int64_t)t * ldz + v] = (T)(rowCoefM[t] * fast_exp2(zhit[e] * k2 - rowL2[t]) - rowCoef[t] * p[e]);
+  const float f = rowFactor[t];
+  const float g = rowCoefM[t] * fast_exp2(zhit[e] * k2 - rowL2[t]) - rowCoef[t] * p[e];
+  dZ[(int64_t)t * ldz + v] = (T)(f != 0.f ? g / f : 0.f);
 }
 
 // l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2) with C_t = sum_k p_k z_{t, idx_k},
@@ -792,7 +875,8 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, int64_t ldz,
                                                     const T* __restrict__ W, int V, int rows,
                                                     int D, int TM, int TN, int ks_total,
-                                                    int split, T* gH, float* partial) {
+                                                    int split, T* gH, float* partial,
+                                                    const float* __restrict__ rowscale) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   const int tiles = TM * TN;
   const int sidx = blockIdx.x / tiles;
@@ -823,7 +907,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
         const int t = m0 + acc_m(wm, i, lane, r);
         if (t < rows) {
           if (split == 1)
-            gH[(int64_t)t * D + d] = (T)acc.v[i][j][r];
+            gH[(int64_t)t * D + d] = (T)(rowscale ? acc.v[i][j][r] * rowscale[t] : acc.v[i][j][r]);
           else
             partial[((int64_t)sidx * rows + t) * D + d] = acc.v[i][j][r];
         }
@@ -832,13 +916,14 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
 }
 
 template <typename T>
-__global__ void k_dh_reduce(const float* partial, int split, int64_t n, T* gH) {
+__global__ void k_dh_reduce(const float* partial, int split, int64_t n, int D,
+                            const float* __restrict__ rowscale, T* gH) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (; i < n; i += stride) {
     float s = 0.f;
     for (int k = 0; k < split; ++k) s += partial[(int64_t)k * n + i];
-    gH[i] = (T)s;
+    gH[i] = (T)(rowscale ? s * rowscale[i / D] : s);
   }
 }
 
@@ -849,7 +934,8 @@ __global__ void k_dh_reduce(const float* partial, int split, int64_t n, T* gH) {
 // per workgroup, 16-byte loads and stores on both sides.
 template <typename T>
 __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H, int tokens,
-                                                         int D, T* __restrict__ Ht, int ldt) {
+                                                         int D, T* __restrict__ Ht, int ldt,
+                                                         const float* __restrict__ rowscale) {
   constexpr int VPT = 16 / (int)sizeof(T);      // elements per 16-byte piece
   constexpr int PAD = 4 / (int)sizeof(T);       // one dword of padding per LDS row
   __shared__ T tile[64][64 + PAD];              // [token][feature]
@@ -864,8 +950,11 @@ __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H,
       v = *reinterpret_cast<const u32x4_t*>(H + (int64_t)(t0 + row) * D + d0 + c);
     T e[VPT];
     __builtin_memcpy(e, &v, 16);
+    // a per-token factor of the gradient rows is applied to the hidden rows
+    // here, so that dW = sum_t (factor_t H_t)^T dZ''_t
+    const float f = (rowscale != nullptr && t0 + row < tokens) ? rowscale[t0 + row] : 1.f;
 #pragma unroll
-    for (int x = 0; x < VPT; ++x) tile[row][c + x] = e[x];
+    for (int x = 0; x < VPT; ++x) tile[row][c + x] = rowscale ? (T)((float)e[x] * f) : e[x];
   }
   __syncthreads();
 #pragma unroll
@@ -1005,12 +1094,12 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 namespace {
 enum ProfKind {
   P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
-  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_RESCALE, P_DZ_TEACHER, P_NKINDS
+  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_FIX, P_DZ_TEACHER, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
     "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
-    "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows", "logits_dz", "dz_rescale",
-    "dz_teacher"};
+    "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows", "logits_dz", "ref_logit",
+    "dz_fix", "dz_teacher"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -1119,27 +1208,32 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     // then the merge of log Z, the rescale of the provisional dZ and its
     // teacher cells
     {
+      ProfScope ps_(P_REF, 0.0, s);
+      hipLaunchKernelGGL(k_ref_logit<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, Hc, W, (int)a.D,
+                         a.tidx, a.tlogit, a.row0, a.rows, a.K, (int)a.V, k2, a.rowR, a.rowFlag);
+    }
+    {
       ProfScope ps_(P_LOGITS_DZ, gemm_flops, s);
       hipLaunchKernelGGL(k_logits_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
                          (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT, a.hits,
-                         a.hoff, a.K, static_cast<T*>(a.dZ), a.ldz, a.zhit);
+                         a.hoff, a.K, static_cast<T*>(a.dZ), a.ldz, a.zhit, a.rowR, a.rowFlag);
     }
     {
       ProfScope ps_(P_MERGE, 0.0, s);
       hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
-                         a.rows, a.nVT, a.rowL2);
+                         a.rows, a.nVT, a.rowL2, a.rowR, a.rowFlag, a.rowCoefM, a.rowMx,
+                         a.rowFactor);
     }
     {
-      ProfScope ps_(P_RESCALE, 0.0, s);
-      const int cb = cdiv(a.ldz, 256 * (16 / (int)sizeof(T)));
-      hipLaunchKernelGGL(k_dz_rescale<T>, dim3(a.rows, cb), dim3(256), 0, s,
-                         static_cast<T*>(a.dZ), a.ldz, a.nVT, a.part_m, a.rowL2, a.rowCoefM);
+      ProfScope ps_(P_FIX, 0.0, s);
+      hipLaunchKernelGGL(k_dz_fix<T>, dim3(a.rows), dim3(256), 0, s, static_cast<T*>(a.dZ), a.ldz,
+                         a.nVT, a.part_m, a.rowR, a.rowFlag, a.rowMx);
     }
     {
       ProfScope ps_(P_DZ_TEACHER, 0.0, s);
       hipLaunchKernelGGL(k_dz_teacher<T>, dim3(cdiv((int64_t)a.rows * a.K, 256)), dim3(256), 0, s,
                          static_cast<T*>(a.dZ), a.ldz, a.tidx, a.p, a.zhit, a.rows, a.K, (int)a.V,
-                         k2, a.rowL2, a.rowCoef, a.rowCoefM);
+                         k2, a.rowL2, a.rowCoef, a.rowCoefM, a.rowFactor);
     }
   } else {
     if (fwd) {
@@ -1154,7 +1248,9 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
       {
         ProfScope ps_(P_MERGE, 0.0, s);
         hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m,
-                           a.part_s, a.rows, a.nVT, a.rowL2);
+                           a.part_s, a.rows, a.nVT, a.rowL2, (const float*)nullptr,
+                           (const int*)nullptr, (const float*)nullptr, (float*)nullptr,
+                           (float*)nullptr);
       }
     }
     if (bwd && !fwd) {
@@ -1190,13 +1286,14 @@ static int launch_dh_impl(const KdDhArgs& a, hipStream_t s) {
     ProfScope ps_(P_DH, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
     hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.split), dim3(kThreads), 0, s,
                        static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.W), (int)a.V,
-                       rows, (int)a.D, TM, TN, ks, a.split, static_cast<T*>(a.gH), a.partial);
+                       rows, (int)a.D, TM, TN, ks, a.split, static_cast<T*>(a.gH), a.partial,
+                       a.rowscale);
   }
   if (a.split > 1) {
     const int64_t n = (int64_t)rows * a.D;
     ProfScope ps_(P_DH_REDUCE, 0.0, s);
     hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256), 0,
-                       s, a.partial, a.split, n, static_cast<T*>(a.gH));
+                       s, a.partial, a.split, n, (int)a.D, a.rowscale, static_cast<T*>(a.gH));
   }
   return (int)hipGetLastError();
 }
@@ -1213,7 +1310,8 @@ static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
   {
     ProfScope ps_(P_TRANSPOSE, 0.0, s);
     hipLaunchKernelGGL(k_transpose_rows<T>, dim3(ldt / 64, (int)(a.D / 64)), dim3(256), 0, s,
-                       static_cast<const T*>(a.Hg), (int)a.tokens, (int)a.D, Ht, ldt);
+                       static_cast<const T*>(a.Hg), (int)a.tokens, (int)a.D, Ht, ldt,
+                       a.rowscale);
   }
   const int TM = cdiv(a.D, kTile), TN = cdiv(a.V, kTile);
   ProfScope ps_(P_DW, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);

@@ -38,6 +38,11 @@ struct KdChunkArgs {
   // per-chunk workspace
   float* p;                 // [rows, K]
   float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
+  float* rowR;              // [rows] reference logit of the single projection
+  int* rowFlag;             // [rows] a tile fell back to its own max
+  float* rowMx;             // [rows] max y of the row
+  float* rowFactor;         // [rows] factor of the row's stored gradient (this
+                            // chunk's rows of the group's factor array)
   float *part_m, *part_s;                            // [rows, nVT]
   int nVT;
   uint32_t* hits;           // [cdiv(rows, 256) * 256 * K] teacher entries by vocab tile
@@ -62,6 +67,7 @@ struct KdDhArgs {
   int split;                // split of the vocabulary (K) range, >= 1
   float* partial;           // [split, tokens, D] when split > 1
   void* gH;                 // grad_hidden + the group's first row * D
+  const float* rowscale;    // [tokens] factor of each dZ row, or null (= 1)
 };
 
 // dW GEMM over the chunks of one group: grad_W (+)= dZ[:tokens]^T H[:tokens]
@@ -75,6 +81,8 @@ struct KdDwArgs {
   void* Ht;                 // workspace for Hg transposed: [D, tokens rounded up to 64]
   int beta;                 // 0 overwrite, 1 accumulate
   float* gW;
+  const float* rowscale;    // [tokens] factor of each dZ row (applied to the
+                            // hidden rows), or null (= 1)
 };
 
 extern "C" {

@@ -82,10 +82,11 @@ def test_backward_matches_oracle(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("N,D,V,K,chunk,tau,ign", SHAPES + [(600, 128, 777, 5, 128, 0.5, 0.1)])
 def test_fused_schedule_matches_split(gpu_lib, dtype, N, D, V, K, chunk, tau, ign):
-    """The fused call projects each chunk once and rescales a provisional dZ;
-    the split entry points recompute the logits (Algorithm 1). Same loss up to
-    the order of the normaliser's fp32 sums; gradients within the fused path's
-    second bf16 rounding of dZ (2^-8 relative), or fp32 rounding."""
+    """The fused call projects each chunk once and stores dZ up to a factor per
+    row (applied to the rows of dH and to the hidden rows for dW); the split
+    entry points recompute the logits (Algorithm 1). Same loss up to the order
+    of the normaliser's fp32 sums; gradients within one more bf16 rounding
+    (2^-8 relative), or within the fp32 gradient tolerance."""
     kd = gpu_lib
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     inp = _inputs(N, D, V, K, tdt, seed=N + 5, ignore_frac=ign)
@@ -95,7 +96,7 @@ def test_fused_schedule_matches_split(gpu_lib, dtype, N, D, V, K, chunk, tau, ig
     torch.cuda.synchronize()
     assert abs(float(fb["loss"]) - float(f["loss"])) <= 1e-6 * abs(float(f["loss"]))
     assert rel_max(to64(fb["loss_per_token"]), to64(f["loss_per_token"])) <= 1e-6
-    gt = 1e-6 if dtype == "f32" else 2.0 ** -7
+    gt = TOL["f32"]["grad"] if dtype == "f32" else 2.0 ** -7
     assert rel_max(to64(fb["grad_hidden"]), to64(b["grad_hidden"])) <= gt
     assert rel_max(to64(fb["grad_W"]), to64(b["grad_W"])) <= gt
 
