@@ -744,9 +744,19 @@ __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, i
   }
   float z = 0.f;
   if (bk < K) {
+    // 16-byte pieces of both rows (D is a multiple of 64, rows 16-byte aligned)
+    constexpr int VPT = 16 / (int)sizeof(T);
     const T* h = Hc + (int64_t)r * D;
     const T* w = W + (int64_t)ix[bk] * D;
-    for (int d = lane; d < D; d += 64) z += (float)h[d] * (float)w[d];
+    for (int d = lane * VPT; d < D; d += 64 * VPT) {
+      const u32x4_t hv = *reinterpret_cast<const u32x4_t*>(h + d);
+      const u32x4_t wv = *reinterpret_cast<const u32x4_t*>(w + d);
+      T he[VPT], we[VPT];
+      __builtin_memcpy(he, &hv, 16);
+      __builtin_memcpy(we, &wv, 16);
+#pragma unroll
+      for (int x = 0; x < VPT; ++x) z += (float)he[x] * (float)we[x];
+    }
     z = wave_sum(z);
   }
   if (lane == 0) {
