@@ -101,6 +101,33 @@ def test_identity_head_closed_form_gradient(gpu_lib):
     _run_and_compare(gpu_lib, inp, tau, 32, TOL["f32"])
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("flag_every", [1, 3])
+def test_reference_logit_fallback(gpu_lib, dtype, flag_every):
+    """The single projection stores 2^(y - R) with R the student logit at the
+    teacher's top entry; a tile whose max exceeds R by more than 2^40 falls
+    back to its own max and its row is rescaled to the row max. W = I puts
+    z = -40 at the top teacher entry and z = +40 in another column of every
+    flag_every-th row (y - R = 80 log2(e) > 40), so those rows take the
+    fallback; the others do not. Loss and gradients against the oracle."""
+    V, K, N, chunk = 512, 6, 96, 64
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, V, V, K, torch.float32, seed=31, hstd=1.0)
+    h = inp["hidden"]
+    idx, logit = inp["teacher_idx"].long(), inp["teacher_logit"]
+    top = idx.gather(1, logit.argmax(dim=1, keepdim=True)).squeeze(1)
+    rows = torch.arange(0, N, flag_every, device="cuda")
+    h[rows, top[rows]] = -40.0
+    # a column outside the row's teacher support gets the large logit
+    far = (top[rows] + V // 2) % V
+    mask = (idx[rows] == far[:, None]).any(dim=1)
+    far = torch.where(mask, (far + 1) % V, far)
+    h[rows, far] = 40.0
+    inp["hidden"] = h.to(tdt).contiguous()
+    inp["W"] = torch.eye(V, dtype=tdt, device="cuda")
+    _run_and_compare(gpu_lib, inp, 1.0, chunk, TOL[dtype])
+
+
 def test_all_ignored(gpu_lib):
     inp = _inputs(200, 64, 600, 5, torch.float32, seed=9)
     inp["ignore"] = torch.ones(200, dtype=torch.uint8, device="cuda")
