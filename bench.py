@@ -3,7 +3,7 @@
 
 One step = one kd_topk_kl_fwd_bwd call over the whole workload: teacher
 prologue, then for every chunk the projection with the online log-normaliser
-and the provisional gradient, the normaliser merge, the gradient rescale with
+and the provisional gradient, the normaliser merge with the per-token factors,
 the teacher correction (Eq. 3), and the dH and dW contractions. The same step
 through the split entry points (forward, then a backward that recomputes the
 logits, as Algorithm 1 does) is timed beside it. Inputs are synthetic (seeded)

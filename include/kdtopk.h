@@ -126,10 +126,11 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  * Schedule: with grad_hidden or grad_W requested, each chunk is projected
  * once. A chunk's log Z is complete once its own projection has run, and the
  * upstream gradient of the mean is known up front, so the projection that
- * yields the normaliser also yields the gradient, with one rescale per
- * (token, vocabulary tile) after the merge of log Z, in place of Algorithm
- * 1's logit recompute (which the split entry points below keep). The
- * transient [chunk, V] buffer is the same one; nothing of size N x V exists.
+ * yields the normaliser also yields the gradient, stored up to a factor per
+ * token that the dH and dW contractions apply once log Z is merged, in place
+ * of Algorithm 1's logit recompute (which the split entry points below
+ * keep). The transient [chunk, V] buffer is the same one; nothing of size
+ * N x V exists. The stream's device must be the current device.
  *
  * Pointers hidden, W, grad_hidden, grad_W and workspace must be 16-byte
  * aligned (KD_ERR_UNSUPPORTED otherwise). hidden, W, teacher_idx,

@@ -2,14 +2,19 @@
 //
 // Per call:    count_valid
 // Per chunk:   teacher_prologue  -> p, M, H, g/tau                 (§3.2, Eq. 2 terms)
-//              logits_lse        -> per (token, vocab tile) max / sum-exp partials
-//              lse_merge         -> log Z per token                 (Alg. 1 normaliser)
 //              bucket            -> teacher entries grouped by vocabulary tile
-//              dz                -> recomputed logits, dZ = g/tau (M q - p), stored
-//                                   row-major [tokens, Vp]; z at the teacher entries
+//   loss and gradients together (one projection per chunk):
+//              ref_logit         -> per-token reference logit R
+//              logits_dz         -> (max, sum-exp) partials per (token, vocab tile),
+//                                   z at the teacher entries, dZ'' = 2^(y - R)
+//              lse_merge         -> log Z and the row factor (g/tau) M 2^(R - log2 Z)
+//              dz_fix, dz_teacher -> fallback rows; teacher cells (Eq. 3) / factor
+//   forward only:  logits_lse (with z at the teacher entries), lse_merge
+//   backward only: dz            -> recomputed logits, dZ = g/tau (M q - p)
 //              row_loss          -> l_t = H - C/tau + M log Z       (Eq. 2)
-//              dh (+ split reduce): dH_c = dZ W
-// Per group of chunks: dw        -> grad_W (+)= dZ^T H (fp32 accumulate)
+//              dh (+ split reduce): dH = dZ W (per chunk or per group; rows scaled
+//                                   by the factor in the one-projection schedule)
+// Per group of chunks: transpose_rows, dw -> grad_W (+)= dZ^T H (fp32 accumulate)
 // Per call:    finalize_loss     -> mean over non-ignored tokens
 #include "kd_device.h"
 #include <type_traits>
@@ -1214,9 +1219,9 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                        (int)a.V, a.nVT, a.hits, a.hitp, a.hoff, a.zhit);
     }
   if (fwd && bwd && a.dZ != nullptr) {
-    // loss and gradients together: one projection per chunk (k_logits_dz),
-    // then the merge of log Z, the rescale of the provisional dZ and its
-    // teacher cells
+    // loss and gradients together: one projection per chunk (k_logits_dz)
+    // against the reference logit, then the merge of log Z with the row
+    // factors, the fallback rows and the teacher cells
     {
       ProfScope ps_(P_REF, 0.0, s);
       hipLaunchKernelGGL(k_ref_logit<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, Hc, W, (int)a.D,
