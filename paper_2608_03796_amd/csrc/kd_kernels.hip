@@ -423,6 +423,11 @@ __device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
 
 // largest exponent (base 2) of a stored provisional gradient 2^(y - R)
 constexpr float kRefGap = 40.f;
+// R is the reference logit plus this many (base 2): stored values are then
+// smaller, which the dH and dW contractions run about 1% faster on (MFMA power
+// depends on the operands); terms below 2^-126 relative to R + kRefShift,
+// i.e. 2^-102 below the reference logit, flush to zero
+constexpr float kRefShift = 24.f;
 
 // epilogue LDS (the main loop's stages are free by then): staging [0, 128 KiB)
 constexpr int kDzBits = kLdsMain;              // 128 x 256-bit hit map of one half
@@ -714,11 +719,11 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
 }
 
 // The reference logit of each token for k_logits_dz: R = z log2(e)/tau at the
-// teacher entry with the largest teacher logit (a valid index), one wave per
-// token; -inf when the row has no valid index. R never exceeds the row's max y
-// beyond rounding, so 2^(y - R) keeps every term that matters; a tile whose max
-// exceeds R by more than kRefGap falls back to its own max. Also clears the
-// row's fallback flag.
+// teacher entry with the largest teacher logit (a valid index), plus
+// kRefShift, one wave per token; -inf when the row has no valid index. The
+// logit part never exceeds the row's max y beyond rounding, so 2^(y - R)
+// keeps every term that matters; a tile whose max exceeds R by more than
+// kRefGap falls back to its own max. Also clears the row's fallback flag.
 template <typename T>
 __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, int D,
                             const int32_t* __restrict__ tidx, const float* __restrict__ tlogit,
@@ -765,7 +770,7 @@ __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, i
     z = wave_sum(z);
   }
   if (lane == 0) {
-    rowR[r] = bk < K ? z * k2 : -INFINITY;
+    rowR[r] = bk < K ? z * k2 + kRefShift : -INFINITY;
     rowFlag[r] = 0;
   }
 }
