@@ -278,10 +278,13 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
 }
 
 // log2 of the normaliser per token from the vocabulary-tile partials (fixed
-// order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau).
+// order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau). A partial
+// is a reference and the sum of 2^(y - reference) over the tile's columns:
+// the tile max (k_logits_lse) or the token's reference logit, or the tile max
+// for a tile that fell back to it (k_logits_dz).
 __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, int nVT,
-                            float* rowL2, const float* rowR, const int* rowFlag,
-                            const float* rowCoefM, float* rowMx, float* rowFactor) {
+                            float* rowL2, const float* rowCoefM, float* rowMx,
+                            float* rowFactor) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
@@ -300,12 +303,12 @@ __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, 
     const float L2 = mx + log2f(s);
     rowL2[r] = L2;
     if (rowFactor != nullptr) {
-      // the factor that turns the row's stored 2^(y - ref) into (g/tau) M q:
-      // ref is the token's reference logit, or its row max when a tile fell
-      // back to its own max (the row is then rescaled to the row max)
-      const float ref = rowFlag[r] ? mx : rowR[r];
+      // the factor that turns the row's stored 2^(y - mx) into (g/tau) M q:
+      // mx is the token's reference logit, the reference of every tile,
+      // unless a tile fell back to its own max (the row's runs are then
+      // rescaled to the largest of their references, mx)
       rowMx[r] = mx;
-      rowFactor[r] = rowCoefM[r] * fast_exp2(ref - L2);
+      rowFactor[r] = rowCoefM[r] * fast_exp2(mx - L2);
     }
   }
 }
@@ -421,8 +424,10 @@ __global__ __launch_bounds__(kBucketThreads) void k_bucket(const int32_t* __rest
 // stores the row of dZ[rows, Vp] (columns V..Vp as zeros).
 __device__ __forceinline__ int hsw16(int n) { return (n ^ (n >> 3)) & 15; }
 
-// largest exponent (base 2) of a stored provisional gradient 2^(y - R)
+// largest exponent (base 2) of the sum of a tile row's stored provisional
+// gradients 2^(y - R), and so of each of them
 constexpr float kRefGap = 40.f;
+constexpr float kRefGapScale = 1099511627776.f;  // 2^kRefGap
 // R is the reference logit plus this many (base 2): stored values are then
 // smaller, which the dH and dW contractions run about 1% faster on (MFMA power
 // depends on the operands); terms below 2^-126 relative to R + kRefShift,
@@ -592,15 +597,16 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
 // A call that wants the loss and its gradients together has each chunk's
 // normaliser complete as soon as that chunk's projection has run, so the
 // chunk is projected once instead of once for log Z and again for dZ: the
-// tile records per token the max m of y = z log2(e) / tau over its columns
-// and the sum of 2^(y - m) (the same partials as k_logits_lse), z at its
-// teacher entries, and the provisional gradient dZ'' = 2^(y - R) in the dZ
-// buffer (0 past V), R being the token's reference logit from k_ref_logit.
+// tile records per token z at its teacher entries, the provisional gradient
+// dZ'' = 2^(y - R) with y = z log2(e) / tau in the dZ buffer (0 past V), R
+// being the token's reference logit from k_ref_logit, and the partials (R,
+// sum of 2^(y - R)) of log Z (a reference and a sum relative to it, like
+// the (max, sum) partials of k_logits_lse).
 // Once log Z is merged, the row factor (g/tau) M 2^(R - log2 Z) turns dZ''
 // into (g/tau) M q; it is applied to the rows of dH and, through the
 // transposed hidden rows, to dW, so dZ'' is never rewritten, except the
 // teacher cells (k_dz_teacher writes (g/tau)(M q - p) / factor, Eq. 3) and the
-// rare rows where a tile's max exceeded R by more than kRefGap (k_dz_fix).
+// rare rows where a tile's sum of 2^(y - R) exceeded 2^kRefGap (k_dz_fix).
 // The [c, V] buffer is the same transient chunk the recompute schedule holds;
 // nothing grows with N. Staging and teacher bookkeeping are those of k_dz.
 template <typename T>
@@ -658,57 +664,78 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
     if (tid < cnt) rec(fe);
     for (int q = kThreads + tid; q < cnt; q += kThreads) rec(hits[seg + hb + q]);
 
-    // 16 lanes per token row, lane lam holding columns 4 lam + 64 k + (0..3):
-    // the row's max m (in base-2 units) and sum of 2^(y - m) reduce within the
-    // 16 lanes (DPP), and 2^(y - m) goes to dZ'' as 128-byte row runs per
-    // store; columns past V give 0 and count for neither
+    // 16 lanes per token row, lane lam holding columns 4 lam + 64 k + (0..3).
+    // The row's run of dZ'' is 2^(y - R) against the token's reference R; the
+    // partials are (R, sum of 2^(y - R)) with the sum reduced within the 16
+    // lanes (DPP). A run whose sum exceeds 2^kRefGap (so its values could
+    // too) is stored against the run's own max m instead, with partials
+    // (m, sum of 2^(y - m)), and its token is flagged for a row rescale.
+    // Columns past V give 0 and count for neither.
 #pragma unroll
     for (int gq = 0; gq < 4; ++gq) {
       const int n = wave * 16 + 4 * gq + rho;  // token row of the half
+      const int t = n0 + 128 * h + n;
       f32x4_t zr[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k)
         zr[k] = *reinterpret_cast<const f32x4_t*>(st + n * 256 + (((lam + 16 * k) ^ hsw16(n)) << 2));
-      float mx = -INFINITY;
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (full || m0 + 4 * lam + 64 * k + e < V) mx = fmaxf(mx, zr[k][e]);
-      const float m = row16_max(mx) * k2;
+      // rows past the chunk use a finite reference (nothing of them is stored)
+      float ref = t < rows ? rowR[t] : 0.f;
       float sum = 0.f;
       f32x4_t G[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          float ev = fast_exp2(zr[k][e] * k2 - m);
+          float ev = fast_exp2(zr[k][e] * k2 - ref);
           if (!full && m0 + 4 * lam + 64 * k + e >= V) ev = 0.f;
           G[k][e] = ev;
           sum += ev;
         }
       sum = row16_sum(sum);
-      const int t = n0 + 128 * h + n;
+      const bool own = !(sum <= kRefGapScale);
+      if (__builtin_amdgcn_ballot_w64(own) != 0ull) {
+        // rare: some row of the wave falls back to its own max (formed for
+        // every row so that the 16-lane reductions run on a full wave)
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (full || m0 + 4 * lam + 64 * k + e < V) mx = fmaxf(mx, zr[k][e]);
+        const float m = row16_max(mx) * k2;
+        float s2 = 0.f;
+        f32x4_t G2[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float ev = fast_exp2(zr[k][e] * k2 - m);
+            if (!full && m0 + 4 * lam + 64 * k + e >= V) ev = 0.f;
+            G2[k][e] = ev;
+            s2 += ev;
+          }
+        s2 = row16_sum(s2);
+        if (own) {
+          ref = m;
+          sum = s2;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) G[k] = G2[k];
+        }
+      }
       if (t < rows) {
-        // stored against the token's reference R (dZ'' = 2^(y - R), at most
-        // 2^kRefGap), or against the tile max m when m exceeds R by more
-        // (the token is then flagged for a row rescale)
-        const float R = rowR[t];
-        const bool own = !(m - R <= kRefGap);
-        const float cmul = own ? 1.f : fast_exp2(m - R);
         T* dst = dZ + (int64_t)t * ldz + m0 + 4 * lam;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const f32x4_t Gs = G[k] * cmul;
           if constexpr (sizeof(T) == 2) {
-            const u32x2_t pk2 = {pack_bf16x2(Gs[0], Gs[1]), pack_bf16x2(Gs[2], Gs[3])};
+            const u32x2_t pk2 = {pack_bf16x2(G[k][0], G[k][1]), pack_bf16x2(G[k][2], G[k][3])};
             *reinterpret_cast<u32x2_t*>(dst + 64 * k) = pk2;
           } else {
-            *reinterpret_cast<f32x4_t*>(dst + 64 * k) = Gs;
+            *reinterpret_cast<f32x4_t*>(dst + 64 * k) = G[k];
           }
         }
         if (lam == 0) {
-          part_m[(int64_t)t * nVT + mt] = m;
+          part_m[(int64_t)t * nVT + mt] = ref;
           part_s[(int64_t)t * nVT + mt] = sum;
           if (own) rowFlag[t] = 1;
         }
@@ -722,8 +749,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
 // teacher entry with the largest teacher logit (a valid index), plus
 // kRefShift, one wave per token; -inf when the row has no valid index. The
 // logit part never exceeds the row's max y beyond rounding, so 2^(y - R)
-// keeps every term that matters; a tile whose max exceeds R by more than
-// kRefGap falls back to its own max. Also clears the row's fallback flag.
+// keeps every term that matters; a tile whose sum of 2^(y - R) exceeds
+// 2^kRefGap falls back to its own max. Also clears the row's fallback flag.
 template <typename T>
 __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, int D,
                             const int32_t* __restrict__ tidx, const float* __restrict__ tlogit,
@@ -776,23 +803,21 @@ __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, i
 }
 
 // Rows whose projection fell back to a tile's own max for some tile: every
-// run of the row is brought to the row max M (2^(ref - M) <= 1 with ref the
-// run's reference), which the row's factor was formed with. One workgroup per
-// row; unflagged rows return at once.
+// run of the row is brought to the largest reference M of the row's runs
+// (2^(ref - M) <= 1 with ref the run's reference), which the row's factor was
+// formed with. One workgroup per row; unflagged rows return at once.
 template <typename T>
 __global__ __launch_bounds__(256) void k_dz_fix(T* __restrict__ dZ, int64_t ldz, int nVT,
                                                 const float* __restrict__ part_m,
-                                                const float* __restrict__ rowR,
                                                 const int* __restrict__ rowFlag,
                                                 const float* __restrict__ rowMx) {
   const int t = blockIdx.x;
   if (rowFlag[t] == 0) return;
   constexpr int VPT = 16 / (int)sizeof(T);
-  const float R = rowR[t], M = rowMx[t];
+  const float M = rowMx[t];
   for (int64_t c0 = (int64_t)threadIdx.x * VPT; c0 < ldz; c0 += 256 * VPT) {
-    const float m = part_m[(int64_t)t * nVT + (c0 >> 8)];
-    const float ref = !(m - R <= kRefGap) ? m : R;
-    const float f = fast_exp2(ref - M);
+    // the run's reference, as its partial recorded it
+    const float f = fast_exp2(part_m[(int64_t)t * nVT + (c0 >> 8)] - M);
     u32x4_t* q = reinterpret_cast<u32x4_t*>(dZ + (int64_t)t * ldz + c0);
     const u32x4_t v = *q;
     // built as a new vector (in-place element updates were miscompiled)
@@ -1241,13 +1266,12 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     {
       ProfScope ps_(P_MERGE, 0.0, s);
       hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
-                         a.rows, a.nVT, a.rowL2, a.rowR, a.rowFlag, a.rowCoefM, a.rowMx,
-                         a.rowFactor);
+                         a.rows, a.nVT, a.rowL2, a.rowCoefM, a.rowMx, a.rowFactor);
     }
     {
       ProfScope ps_(P_FIX, 0.0, s);
       hipLaunchKernelGGL(k_dz_fix<T>, dim3(a.rows), dim3(256), 0, s, static_cast<T*>(a.dZ), a.ldz,
-                         a.nVT, a.part_m, a.rowR, a.rowFlag, a.rowMx);
+                         a.nVT, a.part_m, a.rowFlag, a.rowMx);
     }
     {
       ProfScope ps_(P_DZ_TEACHER, 0.0, s);
@@ -1269,8 +1293,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
         ProfScope ps_(P_MERGE, 0.0, s);
         hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m,
                            a.part_s, a.rows, a.nVT, a.rowL2, (const float*)nullptr,
-                           (const int*)nullptr, (const float*)nullptr, (float*)nullptr,
-                           (float*)nullptr);
+                           (float*)nullptr, (float*)nullptr);
       }
     }
     if (bwd && !fwd) {

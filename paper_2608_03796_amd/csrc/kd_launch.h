@@ -40,7 +40,7 @@ struct KdChunkArgs {
   float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
   float* rowR;              // [rows] reference logit of the single projection
   int* rowFlag;             // [rows] a tile fell back to its own max
-  float* rowMx;             // [rows] max y of the row
+  float* rowMx;             // [rows] largest tile reference of the row
   float* rowFactor;         // [rows] factor of the row's stored gradient (this
                             // chunk's rows of the group's factor array)
   float *part_m, *part_s;                            // [rows, nVT]

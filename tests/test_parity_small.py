@@ -105,11 +105,12 @@ def test_identity_head_closed_form_gradient(gpu_lib):
 @pytest.mark.parametrize("flag_every", [1, 3])
 def test_reference_logit_fallback(gpu_lib, dtype, flag_every):
     """The single projection stores 2^(y - R) with R the student logit at the
-    teacher's top entry; a tile whose max exceeds R by more than 2^40 falls
-    back to its own max and its row is rescaled to the row max. W = I puts
-    z = -40 at the top teacher entry and z = +40 in another column of every
-    flag_every-th row (y - R = 80 log2(e) > 40), so those rows take the
-    fallback; the others do not. Loss and gradients against the oracle."""
+    teacher's top entry; a tile row whose sum of 2^(y - R) exceeds 2^40 falls
+    back to its own max and its row is rescaled to the largest reference of
+    its runs. W = I puts z = -40 at the top teacher entry and z = +40 in
+    another column of every flag_every-th row (y - R = 80 log2(e) - 24 > 40),
+    so those rows take the fallback; the others do not. Loss and gradients
+    against the oracle."""
     V, K, N, chunk = 512, 6, 96, 64
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     inp = _inputs(N, V, V, K, torch.float32, seed=31, hstd=1.0)
