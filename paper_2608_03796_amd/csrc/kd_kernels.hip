@@ -629,6 +629,10 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
   const int* ho = hoff + (int64_t)nt * (nVT + 1) + mt;
   const int hb = ho[0], cnt = ho[1] - hb;
   const uint32_t fe = tid < cnt ? hits[seg + hb + tid] : 0u;
+  // the tile's reference logits, loaded before the main loop: a load issued
+  // in the epilogue would wait for every store issued before it (loads and
+  // stores complete in order), serialising the row pass on its stores
+  const float rref = (tid < kTile && n0 + tid < rows) ? rowR[n0 + tid] : 0.f;
 
   AccTile acc;
   gemm_tile<T, KcOp, KcOp, 8, false, 3>(
@@ -638,6 +642,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
   const bool full = m0 + kTile <= V;
 
   float* st = reinterpret_cast<float*>(lds);
+  // past the staging area: R of the tile's 256 tokens (0 past the chunk)
+  float* rs_r = reinterpret_cast<float*>(lds + kLdsMain);
+  if (tid < kTile) rs_r[tid] = rref;
   const int rho = lane >> 4, lam = lane & 15;  // row pass: 4 token rows per wave, 16 lanes each
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -680,7 +687,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
       for (int k = 0; k < 4; ++k)
         zr[k] = *reinterpret_cast<const f32x4_t*>(st + n * 256 + (((lam + 16 * k) ^ hsw16(n)) << 2));
       // rows past the chunk use a finite reference (nothing of them is stored)
-      float ref = t < rows ? rowR[t] : 0.f;
+      float ref = rs_r[128 * h + n];
       float sum = 0.f;
       f32x4_t G[4];
 #pragma unroll
@@ -934,29 +941,41 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const int kb = sidx * per, ke = min(ks_total, kb + per);
   AccTile acc;
   const int mrows = min(kTile, rows - m0);
+  // the row factors of the tile's 256 rows, loaded before the main loop and
+  // kept in LDS for the epilogue: a load there would wait for every store
+  // issued before it (loads and stores complete in order)
+  const int tid = threadIdx.x;
+  const float rsv =
+      (rowscale != nullptr && split == 1 && tid < kTile && m0 + tid < rows) ? rowscale[m0 + tid]
+                                                                           : 1.f;
   gemm_tile<T, KcOp, KmOp, 8, true, 3>(
       KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
                KmOp{reinterpret_cast<const char*>(W + n0),
                     (int64_t)V * ldb - (int64_t)n0 * eb, ldb},
                kb, ke, lds, acc);
-  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int lane = tid & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
+  float* rsl = reinterpret_cast<float*>(lds);
+  if (tid < kTile) rsl[tid] = rsv;
+  __syncthreads();
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int d = n0 + acc_n(wn, j, lane);
-    if (d >= D) continue;
+  for (int i = 0; i < 8; ++i) {
+    const f32x4_t sc = *reinterpret_cast<const f32x4_t*>(rsl + acc_m(wm, i, lane, 0));
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int j = 0; j < 4; ++j) {
+      const int d = n0 + acc_n(wn, j, lane);
+      if (d >= D) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = m0 + acc_m(wm, i, lane, r);
         if (t < rows) {
           if (split == 1)
-            gH[(int64_t)t * D + d] = (T)(rowscale ? acc.v[i][j][r] * rowscale[t] : acc.v[i][j][r]);
+            gH[(int64_t)t * D + d] = (T)(acc.v[i][j][r] * sc[r]);
           else
             partial[((int64_t)sidx * rows + t) * D + d] = acc.v[i][j][r];
         }
       }
+    }
   }
 }
 

@@ -103,22 +103,27 @@ def test_identity_head_closed_form_gradient(gpu_lib):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("flag_every", [1, 3])
-def test_reference_logit_fallback(gpu_lib, dtype, flag_every):
+@pytest.mark.parametrize("top_z", [-40.0, -20.0])
+@pytest.mark.parametrize("V", [512, 640])
+def test_reference_logit_fallback(gpu_lib, dtype, flag_every, top_z, V):
     """The single projection stores 2^(y - R) with R the student logit at the
-    teacher's top entry; a tile row whose sum of 2^(y - R) exceeds 2^40 falls
-    back to its own max and its row is rescaled to the largest reference of
-    its runs. W = I puts z = -40 at the top teacher entry and z = +40 in
-    another column of every flag_every-th row (y - R = 80 log2(e) - 24 > 40),
-    so those rows take the fallback; the others do not. Loss and gradients
+    teacher's top entry (+24, base 2); a tile row whose sum of 2^(y - R)
+    exceeds 2^40 falls back to its own max and its row is rescaled to the
+    largest reference of its runs. W = I puts z = top_z at the top teacher
+    entry and z = +40 in another column of every flag_every-th row. With
+    top_z = -40 every tile of those rows falls back (its ordinary columns
+    alone sum past 2^40); with top_z = -20 only the tile holding the +40
+    column does, so a row mixes runs stored against R and against a tile
+    max. V = 640 leaves a partial last vocabulary tile. Loss and gradients
     against the oracle."""
-    V, K, N, chunk = 512, 6, 96, 64
+    K, N, chunk = 6, 96, 64
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     inp = _inputs(N, V, V, K, torch.float32, seed=31, hstd=1.0)
     h = inp["hidden"]
     idx, logit = inp["teacher_idx"].long(), inp["teacher_logit"]
     top = idx.gather(1, logit.argmax(dim=1, keepdim=True)).squeeze(1)
     rows = torch.arange(0, N, flag_every, device="cuda")
-    h[rows, top[rows]] = -40.0
+    h[rows, top[rows]] = top_z
     # a column outside the row's teacher support gets the large logit
     far = (top[rows] + V // 2) % V
     mask = (idx[rows] == far[:, None]).any(dim=1)
