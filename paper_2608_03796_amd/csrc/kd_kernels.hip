@@ -688,17 +688,24 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
         zr[k] = *reinterpret_cast<const f32x4_t*>(st + n * 256 + (((lam + 16 * k) ^ hsw16(n)) << 2));
       // rows past the chunk use a finite reference (nothing of them is stored)
       float ref = rs_r[128 * h + n];
-      float sum = 0.f;
       f32x4_t G[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k)
+        G[k] = f32x4_t{fast_exp2(zr[k][0] * k2 - ref), fast_exp2(zr[k][1] * k2 - ref),
+                       fast_exp2(zr[k][2] * k2 - ref), fast_exp2(zr[k][3] * k2 - ref)};
+      // the column mask only on the last vocabulary tile (a wave-uniform
+      // branch instead of per-element selects on every tile)
+      if (!full) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float ev = fast_exp2(zr[k][e] * k2 - ref);
-          if (!full && m0 + 4 * lam + 64 * k + e >= V) ev = 0.f;
-          G[k][e] = ev;
-          sum += ev;
+        for (int k = 0; k < 4; ++k) {
+          const int c = m0 + 4 * lam + 64 * k;
+          G[k] = f32x4_t{c < V ? G[k][0] : 0.f, c + 1 < V ? G[k][1] : 0.f,
+                         c + 2 < V ? G[k][2] : 0.f, c + 3 < V ? G[k][3] : 0.f};
         }
+      }
+      float sum = 0.f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) sum += (G[k][0] + G[k][1]) + (G[k][2] + G[k][3]);
       sum = row16_sum(sum);
       const bool own = !(sum <= kRefGapScale);
       if (__builtin_amdgcn_ballot_w64(own) != 0ull) {
