@@ -232,12 +232,15 @@ kd_status kd_topk_kl_check_indices(const kd_problem* p,
 
 /*
  * Instrumentation, not part of the method: per-kernel timing with HIP events.
- * While enabled (process-wide), kd_topk_kl_fwd_bwd records a HIP event pair on
- * its stream around each kernel launch; kd_profile_read waits for the recorded
+ * kd_profile_enable(mode), process-wide: 0 off; 1 the entry points record a
+ * HIP event pair on their stream around each kernel launch; 2 only around the
+ * contraction kernels (the projection, dH and dW launches, whose `flops` is
+ * nonzero), which keeps the events' own cost out of the rest of the step.
+ * Another mode gives KD_ERR_BAD_ARG. kd_profile_read waits for the recorded
  * events, writes up to `max` entries (one per kernel kind that ran), clears the
  * records and returns the number of entries written (negative on a HIP error).
  * `flops` is the algorithmic floating-point work of the recorded launches (the
- * four 2*rows*D*V contractions of each chunk; 0 for the other kernels).
+ * 2*rows*D*V contractions of each chunk; 0 for the other kernels).
  * Creating events is an allocation: leave profiling off where that matters.
  */
 typedef struct kd_kernel_time {
@@ -247,7 +250,7 @@ typedef struct kd_kernel_time {
   double flops;        /* sum of algorithmic FLOP over the launches */
 } kd_kernel_time;
 
-kd_status kd_profile_enable(int on);
+kd_status kd_profile_enable(int mode);
 int kd_profile_read(kd_kernel_time* out, int max);
 
 /* Static, NUL-terminated description of a status code (never NULL). */

@@ -374,9 +374,12 @@ def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, work
     return True
 
 
-def profile_enable(on: bool = True):
-    """Per-kernel HIP-event timing inside the library (instrumentation)."""
-    load_library().kd_profile_enable(int(bool(on)))
+def profile_enable(on: bool = True, contractions_only: bool = False):
+    """Per-kernel HIP-event timing inside the library (instrumentation): off,
+    around every kernel, or only around the contraction kernels."""
+    rc = load_library().kd_profile_enable(0 if not on else (2 if contractions_only else 1))
+    if rc != 0:
+        raise KdError(rc, "kd_profile_enable")
 
 
 def profile_read() -> dict:

@@ -1176,7 +1176,7 @@ struct ProfRec {
   hipEvent_t a, b;
   double flops;
 };
-std::atomic<bool> g_prof_on{false};
+std::atomic<int> g_prof_mode{0};  // 0 off, 1 every kernel, 2 contractions only
 std::mutex g_prof_mu;
 std::vector<ProfRec> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
@@ -1199,7 +1199,8 @@ struct ProfScope {
   hipStream_t s;
   hipEvent_t a = nullptr;
   ProfScope(int k, double f, hipStream_t st) : kind(k), flops(f), s(st) {
-    if (!g_prof_on.load(std::memory_order_relaxed)) return;
+    const int mode = g_prof_mode.load(std::memory_order_relaxed);
+    if (mode == 0 || (mode == 2 && f == 0.0)) return;
     std::lock_guard<std::mutex> g(g_prof_mu);
     a = prof_event();
     if (a) (void)hipEventRecord(a, s);
@@ -1218,8 +1219,9 @@ struct ProfScope {
 };
 }  // namespace
 
-extern "C" kd_status kd_profile_enable(int on) {
-  g_prof_on.store(on != 0);
+extern "C" kd_status kd_profile_enable(int mode) {
+  if (mode < 0 || mode > 2) return KD_ERR_BAD_ARG;
+  g_prof_mode.store(mode);
   return KD_OK;
 }
 

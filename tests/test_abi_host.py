@@ -45,6 +45,17 @@ def test_status_strings(lib):
     assert lib.kd_status_string(99) == b"unknown kd_status"
 
 
+def test_profile_modes(lib):
+    """0 off, 1 every kernel, 2 contraction kernels only; anything else is
+    rejected. Setting a mode touches no device; reading with nothing recorded
+    returns no entries."""
+    for mode in (1, 2, 0):
+        assert lib.kd_profile_enable(mode) == 0
+    for bad in (-1, 3):
+        assert lib.kd_profile_enable(bad) == 3  # KD_ERR_BAD_ARG
+    assert lib.kd_profile_read((kd.KdKernelTime * 4)(), 4) == 0
+
+
 def _prob(**kw):
     base = dict(N=256, D=256, V=4096, K=16, chunk=64, tau=1.0, dtype=kd.KD_F32)
     base.update(kw)
