@@ -33,7 +33,7 @@ struct Plan {
   int64_t Vp;          // V rounded up to the 256-column tile
   int64_t nVT;         // vocabulary tiles
   int64_t nchunks;
-  int64_t nblk;        // loss partials of a full chunk (one per 16 rows)
+  int64_t nblk;        // loss partials of a full chunk (one per kLossRows rows)
   int64_t G;           // chunks whose dZ rows are gathered before one dH and one dW GEMM
   int64_t ngroups;
   bool dh_per_group;   // dH once per group (a chunk alone has too few tiles) or per chunk
@@ -84,7 +84,7 @@ Plan make_plan(const kd_problem* p) {
   pl.Vp = rup(pl.V, kTile);
   pl.nVT = pl.Vp / kTile;
   pl.nchunks = cdiv(pl.N, pl.c);
-  pl.nblk = cdiv(pl.c, 16);
+  pl.nblk = cdiv(pl.c, kLossRows);
   // dW is accumulated in fp32 in place: each dW GEMM reads and writes all of
   // grad_W once, so gather the dZ rows of up to ~16384 tokens (and at most
   // 4 GiB of dZ) per GEMM
@@ -114,7 +114,7 @@ Plan make_plan(const kd_problem* p) {
   };
   pl.off_misc = take(256);
   pl.off_p = take((size_t)pl.cp * pl.K * 4);
-  pl.off_rows = take((size_t)8 * pl.cp * 4);
+  pl.off_rows = take((size_t)7 * pl.cp * 4);
   pl.off_pm = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_hits = take((size_t)pl.cp * pl.K * 4);
@@ -269,8 +269,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.rowCoefM = rows + 3 * pl.cp;
     a.rowL2 = rows + 4 * pl.cp;
     a.rowR = rows + 5 * pl.cp;
-    a.rowMx = rows + 6 * pl.cp;
-    a.rowFlag = reinterpret_cast<int*>(rows + 7 * pl.cp);
+    a.rowFlag = reinterpret_cast<int*>(rows + 6 * pl.cp);
     a.part_m = reinterpret_cast<float*>(ws + pl.off_pm);
     a.part_s = reinterpret_cast<float*>(ws + pl.off_ps);
     a.hits = reinterpret_cast<uint32_t*>(ws + pl.off_hits);
@@ -285,7 +284,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.loss_per_token = c.lpt ? c.lpt + row0 : nullptr;
     a.block_partial = lossp + n_partials;
     if (kd_launch_chunk(&a, c.stream) != 0) return KD_ERR_DEVICE;
-    n_partials += cdiv(rcount, 16);
+    n_partials += cdiv(rcount, kLossRows);
     group_tokens += rcount;
     // dH over rows [r0, r0 + n) of the dZ buffer (from its row `zrow`)
     auto dh = [&](int64_t r0, int64_t n, int64_t zrow) -> bool {

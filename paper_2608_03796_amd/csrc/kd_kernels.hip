@@ -278,13 +278,10 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
 }
 
 // log2 of the normaliser per token from the vocabulary-tile partials (fixed
-// order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau). A partial
-// is a reference and the sum of 2^(y - reference) over the tile's columns:
-// the tile max (k_logits_lse) or the token's reference logit, or the tile max
-// for a tile that fell back to it (k_logits_dz).
+// order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau); a partial
+// is the tile max and the sum of 2^(y - max) over the tile's columns.
 __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, int nVT,
-                            float* rowL2, const float* rowCoefM, float* rowMx,
-                            float* rowFactor) {
+                            float* rowL2) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
@@ -299,18 +296,7 @@ __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, 
     if (m != -INFINITY) s += ps[j] * fast_exp2(m - mx);
   }
   s = wave_sum(s);
-  if (lane == 0) {
-    const float L2 = mx + log2f(s);
-    rowL2[r] = L2;
-    if (rowFactor != nullptr) {
-      // the factor that turns the row's stored 2^(y - mx) into (g/tau) M q:
-      // mx is the token's reference logit, the reference of every tile,
-      // unless a tile fell back to its own max (the row's runs are then
-      // rescaled to the largest of their references, mx)
-      rowMx[r] = mx;
-      rowFactor[r] = rowCoefM[r] * fast_exp2(mx - L2);
-    }
-  }
+  if (lane == 0) rowL2[r] = mx + log2f(s);
 }
 
 // ------------------------------------------------ teacher entry buckets ----
@@ -816,98 +802,119 @@ __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, i
   }
 }
 
-// Rows whose projection fell back to a tile's own max for some tile: every
-// run of the row is brought to the largest reference M of the row's runs
-// (2^(ref - M) <= 1 with ref the run's reference), which the row's factor was
-// formed with. One workgroup per row; unflagged rows return at once.
-template <typename T>
-__global__ __launch_bounds__(256) void k_dz_fix(T* __restrict__ dZ, int64_t ldz, int nVT,
-                                                const float* __restrict__ part_m,
-                                                const int* __restrict__ rowFlag,
-                                                const float* __restrict__ rowMx) {
-  const int t = blockIdx.x;
-  if (rowFlag[t] == 0) return;
-  constexpr int VPT = 16 / (int)sizeof(T);
-  const float M = rowMx[t];
-  for (int64_t c0 = (int64_t)threadIdx.x * VPT; c0 < ldz; c0 += 256 * VPT) {
-    // the run's reference, as its partial recorded it
-    const float f = fast_exp2(part_m[(int64_t)t * nVT + (c0 >> 8)] - M);
-    u32x4_t* q = reinterpret_cast<u32x4_t*>(dZ + (int64_t)t * ldz + c0);
-    const u32x4_t v = *q;
-    // built as a new vector (in-place element updates were miscompiled)
-    if constexpr (sizeof(T) == 2) {
-      uint32_t o[4];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const uint32_t x = v[w];
-        o[w] = pack_bf16x2(__builtin_bit_cast(float, x << 16) * f,
-                           __builtin_bit_cast(float, x & 0xffff0000u) * f);
-      }
-      *q = u32x4_t{o[0], o[1], o[2], o[3]};
-    } else {
-      *q = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) * f);
-    }
-  }
-}
-
-// The teacher cells of dZ: (g/tau) M 2^(z log2(e)/tau - log2 Z) - (g/tau) p in
-// the row's stored scale (divided by the row factor; 0 where the factor is 0,
-// i.e. on ignored rows), one thread per entry of the chunk (indices outside
-// [0, V) are skipped).
-template <typename T>
-__global__ __launch_bounds__(256) void k_dz_teacher(T* __restrict__ dZ, int64_t ldz,
-                                                    const int32_t* __restrict__ tidx,
-                                                    const float* __restrict__ p,
-                                                    const float* __restrict__ zhit, int rows,
-                                                    int K, int V, float k2,
-                                                    const float* __restrict__ rowL2,
-                                                    const float* __restrict__ rowCoef,
-                                                    const float* __restrict__ rowCoefM,
-                                                    const float* __restrict__ rowFactor) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= (int64_t)rows * K) return;
-  const int v = tidx[e];
-  if ((unsigned)v >= (unsigned)V) return;
-  const int t = (int)(e / K);
-  const float f = rowFactor[t];
-  const float g = rowCoefM[t] * fast_exp2(zhit[e] * k2 - rowL2[t]) - rowCoef[t] * p[e];
-  dZ[(int64_t)t * ldz + v] = (T)(f != 0.f ? g / f : 0.f);
-}
-
 // l_t = H_t - C_t / tau + M_t log Z_t (Eq. 2) with C_t = sum_k p_k z_{t, idx_k},
-// 0 on ignored rows; per-block partial sums in a fixed order for the
-// deterministic mean.
-constexpr int kLossRows = 16;  // rows per row-loss block (4 per wave)
+// 0 on ignored rows; one wave per row and a partial sum per block of
+// kLossRows rows in a fixed order, for the deterministic mean.
 __global__ void k_row_loss(const float* zhit, const float* p, int K, const float* rowL2,
                            const float* rowM, const float* rowH, const uint8_t* ignore,
                            int64_t row0, int rows, float inv_tau, float* loss_per_token,
                            float* logz_out, float* block_partial) {
-  // one fixed-order partial per block
-  __shared__ float red[4];
+  __shared__ float red[kLossRows];
   const int lane = threadIdx.x & 63, wave = wave_id();
-  float c[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int k = lane; k < K; k += 64) {
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int r = blockIdx.x * kLossRows + wave * 4 + rr;
-      if (r < rows) c[rr] += p[(int64_t)r * K + k] * zhit[(int64_t)r * K + k];
-    }
-  }
-  float acc = 0.f;
-#pragma unroll
-  for (int rr = 0; rr < 4; ++rr) {
-    const int r = blockIdx.x * kLossRows + wave * 4 + rr;
-    const float cs = wave_sum(c[rr]);
-    if (r >= rows) continue;
+  const int r = blockIdx.x * kLossRows + wave;
+  float l = 0.f;
+  if (r < rows) {
+    float c = 0.f;
+    for (int k = lane; k < K; k += 64) c += p[(int64_t)r * K + k] * zhit[(int64_t)r * K + k];
+    c = wave_sum(c);
     const bool valid = ignore == nullptr || ignore[row0 + r] == 0;
-    const float l = valid ? rowH[r] - cs * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
+    l = valid ? rowH[r] - c * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
     if (lane == 0) {
       if (loss_per_token) loss_per_token[r] = l;
       if (logz_out) logz_out[r] = rowL2[r] * kLn2;
-      acc += l;
     }
   }
-  if (lane == 0) red[wave] = acc;
+  if (lane == 0) red[wave] = l;
+  __syncthreads();
+  if (threadIdx.x == 0) block_partial[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// The end of a chunk in the single-projection schedule, one wave per token
+// (one pass instead of four launches): log2 Z merged from the tile partials
+// (each a reference and a sum relative to it), the row factor that turns the
+// stored 2^(y - mx) into (g/tau) M q, mx being the largest reference of the
+// row's tiles (the token's reference logit unless a tile fell back to its own
+// max); for a row with such a tile, every run brought to mx; the teacher
+// cells (g/tau)(M q - p) (Eq. 3) in the row's stored scale (0 where the
+// factor is 0, i.e. on ignored rows); and the token's loss (Eq. 2) with a
+// partial per block of kLossRows rows as k_row_loss forms it.
+template <typename T>
+__global__ __launch_bounds__(256) void k_row_finish(
+    const float* __restrict__ part_m, const float* __restrict__ part_s, int nVT,
+    const int* __restrict__ rowFlag, T* dZ, int64_t ldz, const int32_t* __restrict__ tidx,
+    const float* __restrict__ p, const float* __restrict__ zhit, int K, int V, float k2,
+    const float* __restrict__ rowM, const float* __restrict__ rowH,
+    const float* __restrict__ rowCoef, const float* __restrict__ rowCoefM,
+    const uint8_t* __restrict__ ignore, int64_t row0, int rows, float inv_tau, float* rowL2,
+    float* rowFactor, float* loss_per_token, float* block_partial) {
+  __shared__ float red[kLossRows];
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int r = blockIdx.x * kLossRows + wave;
+  float l = 0.f;
+  if (r < rows) {
+    const float* pm = part_m + (int64_t)r * nVT;
+    const float* ps = part_s + (int64_t)r * nVT;
+    float mx = -INFINITY;
+    for (int j = lane; j < nVT; j += 64) mx = fmaxf(mx, pm[j]);
+    mx = wave_max(mx);
+    float s = 0.f;
+    for (int j = lane; j < nVT; j += 64) {
+      const float m = pm[j];
+      if (m != -INFINITY) s += ps[j] * fast_exp2(m - mx);
+    }
+    s = wave_sum(s);
+    const float L2 = mx + log2f(s);
+    const float cm = rowCoefM[r], cf = rowCoef[r];
+    const float f = cm * fast_exp2(mx - L2);
+    if (lane == 0) {
+      rowL2[r] = L2;
+      rowFactor[r] = f;
+    }
+    T* row = dZ + (int64_t)r * ldz;
+    if (rowFlag[r] != 0) {
+      // rare: runs stored against different references
+      constexpr int VPT = 16 / (int)sizeof(T);
+      for (int64_t c0 = (int64_t)lane * VPT; c0 < ldz; c0 += 64 * VPT) {
+        const float fr = fast_exp2(pm[c0 >> 8] - mx);
+        u32x4_t* q = reinterpret_cast<u32x4_t*>(row + c0);
+        const u32x4_t v = *q;
+        // built as a new vector (in-place element updates were miscompiled)
+        if constexpr (sizeof(T) == 2) {
+          uint32_t o[4];
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t x = v[w];
+            o[w] = pack_bf16x2(__builtin_bit_cast(float, x << 16) * fr,
+                               __builtin_bit_cast(float, x & 0xffff0000u) * fr);
+          }
+          *q = u32x4_t{o[0], o[1], o[2], o[3]};
+        } else {
+          *q = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) * fr);
+        }
+      }
+      // the teacher cells below overwrite some of these elements: the wave's
+      // rescale stores complete first (a workgroup-scope fence emits no wait
+      // here, so the wait is explicit; the clobber keeps the compiler from
+      // moving memory accesses across it)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    float c = 0.f;
+    for (int k = lane; k < K; k += 64) {
+      const int64_t e = (int64_t)r * K + k;
+      const float pk = p[e], z = zhit[e];
+      c += pk * z;
+      const int v = tidx[e];
+      if ((unsigned)v < (unsigned)V) {
+        const float g = cm * fast_exp2(z * k2 - L2) - cf * pk;
+        row[v] = (T)(f != 0.f ? g / f : 0.f);
+      }
+    }
+    c = wave_sum(c);
+    const bool valid = ignore == nullptr || ignore[row0 + r] == 0;
+    l = valid ? rowH[r] - c * inv_tau + rowM[r] * L2 * kLn2 : 0.f;
+    if (lane == 0 && loss_per_token) loss_per_token[r] = l;
+  }
+  if (lane == 0) red[wave] = l;
   __syncthreads();
   if (threadIdx.x == 0) block_partial[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
 }
@@ -1165,12 +1172,12 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 namespace {
 enum ProfKind {
   P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
-  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_FIX, P_DZ_TEACHER, P_NKINDS
+  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_ROW_FINISH, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
     "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
     "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows", "logits_dz", "ref_logit",
-    "dz_fix", "dz_teacher"};
+    "row_finish"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -1279,7 +1286,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
   if (fwd && bwd && a.dZ != nullptr) {
     // loss and gradients together: one projection per chunk (k_logits_dz)
     // against the reference logit, then the merge of log Z with the row
-    // factors, the fallback rows and the teacher cells
+    // factors, the fallback rows, the teacher cells and the row losses
     {
       ProfScope ps_(P_REF, 0.0, s);
       hipLaunchKernelGGL(k_ref_logit<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, Hc, W, (int)a.D,
@@ -1292,20 +1299,12 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                          a.hoff, a.K, static_cast<T*>(a.dZ), a.ldz, a.zhit, a.rowR, a.rowFlag);
     }
     {
-      ProfScope ps_(P_MERGE, 0.0, s);
-      hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m, a.part_s,
-                         a.rows, a.nVT, a.rowL2, a.rowCoefM, a.rowMx, a.rowFactor);
-    }
-    {
-      ProfScope ps_(P_FIX, 0.0, s);
-      hipLaunchKernelGGL(k_dz_fix<T>, dim3(a.rows), dim3(256), 0, s, static_cast<T*>(a.dZ), a.ldz,
-                         a.nVT, a.part_m, a.rowFlag, a.rowMx);
-    }
-    {
-      ProfScope ps_(P_DZ_TEACHER, 0.0, s);
-      hipLaunchKernelGGL(k_dz_teacher<T>, dim3(cdiv((int64_t)a.rows * a.K, 256)), dim3(256), 0, s,
-                         static_cast<T*>(a.dZ), a.ldz, a.tidx, a.p, a.zhit, a.rows, a.K, (int)a.V,
-                         k2, a.rowL2, a.rowCoef, a.rowCoefM, a.rowFactor);
+      ProfScope ps_(P_ROW_FINISH, 0.0, s);
+      hipLaunchKernelGGL(k_row_finish<T>, dim3(cdiv(a.rows, kLossRows)), dim3(64 * kLossRows), 0,
+                         s, a.part_m, a.part_s, a.nVT, a.rowFlag, static_cast<T*>(a.dZ), a.ldz,
+                         a.tidx, a.p, a.zhit, a.K, (int)a.V, k2, a.rowM, a.rowH, a.rowCoef,
+                         a.rowCoefM, a.ignore, a.row0, a.rows, a.inv_tau, a.rowL2, a.rowFactor,
+                         a.loss_per_token, a.block_partial);
     }
   } else {
     if (fwd) {
@@ -1320,8 +1319,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
       {
         ProfScope ps_(P_MERGE, 0.0, s);
         hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m,
-                           a.part_s, a.rows, a.nVT, a.rowL2, (const float*)nullptr,
-                           (float*)nullptr, (float*)nullptr);
+                           a.part_s, a.rows, a.nVT, a.rowL2);
       }
     }
     if (bwd && !fwd) {
@@ -1333,12 +1331,12 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
                          a.hitp, a.hoff, a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz,
                          (float*)nullptr);
     }
-  }
-  if (fwd) {
-    ProfScope ps_(P_ROW_LOSS, 0.0, s);
-    hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(256), 0, s, a.zhit, a.p,
-                       a.K, a.rowL2, a.rowM, a.rowH, a.ignore, a.row0, a.rows, a.inv_tau,
-                       a.loss_per_token, a.logz_out, a.block_partial);
+    if (fwd) {
+      ProfScope ps_(P_ROW_LOSS, 0.0, s);
+      hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(64 * kLossRows), 0, s,
+                         a.zhit, a.p, a.K, a.rowL2, a.rowM, a.rowH, a.ignore, a.row0, a.rows,
+                         a.inv_tau, a.loss_per_token, a.logz_out, a.block_partial);
+    }
   }
   return (int)hipGetLastError();
 }

@@ -16,6 +16,9 @@ struct KdPrepareArgs {
 
 enum { KD_MODE_FWD_BWD = 0, KD_MODE_FWD = 1, KD_MODE_BWD = 2 };
 
+// tokens per loss partial (one block of the row-loss kernels, a wave per token)
+constexpr int kLossRows = 4;
+
 struct KdChunkArgs {
   int dtype;
   int mode;                 // KD_MODE_*: which half of Algorithm 1 runs
@@ -40,7 +43,6 @@ struct KdChunkArgs {
   float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
   float* rowR;              // [rows] reference logit of the single projection
   int* rowFlag;             // [rows] a tile fell back to its own max
-  float* rowMx;             // [rows] largest tile reference of the row
   float* rowFactor;         // [rows] factor of the row's stored gradient (this
                             // chunk's rows of the group's factor array)
   float *part_m, *part_s;                            // [rows, nVT]
@@ -53,7 +55,7 @@ struct KdChunkArgs {
   int64_t ldz;              // = padded vocabulary (columns V..ldz: finite, z = 0 there)
   // outputs
   float* loss_per_token;    // + row0, or null
-  float* block_partial;     // this chunk's cdiv(rows, 16) partial sums
+  float* block_partial;     // this chunk's cdiv(rows, kLossRows) partial sums
 };
 
 // dH GEMM over the chunks of one group: grad_hidden[rows] = dZ[rows] W
