@@ -148,15 +148,22 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}))
 
 
-def kernel_sources_sha256():
-    """Digest of the HIP sources, to tell whether stored counters still apply."""
+def kernel_sources_sha256(csrc_dir=None):
+    """Digest of the HIP sources' code, to tell whether stored counters still
+    apply: comments and layout are left out, so that editing a comment keeps
+    the counters taken on the same code."""
     import hashlib
-    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_03796_amd", "csrc")
+    import re
+    d = csrc_dir or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                 "paper_2608_03796_amd", "csrc")
+    tok = re.compile(r'"(?:\\.|[^"\\])*"|\'(?:\\.|[^\'\\])*\'|//[^\n]*|/\*.*?\*/', re.S)
     h = hashlib.sha256()
     for name in sorted(os.listdir(d)):
         if name.endswith((".hip", ".h", ".cpp")):
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+            with open(os.path.join(d, name)) as f:
+                text = f.read()
+            code = tok.sub(lambda m: m.group(0) if m.group(0)[0] in "\"'" else " ", text)
+            h.update(name.encode() + b"\0" + " ".join(code.split()).encode())
     return h.hexdigest()
 
 

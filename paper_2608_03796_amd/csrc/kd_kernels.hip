@@ -5,13 +5,13 @@
 //              bucket            -> teacher entries grouped by vocabulary tile
 //   loss and gradients together (one projection per chunk):
 //              ref_logit         -> per-token reference logit R
-//              logits_dz         -> (max, sum-exp) partials per (token, vocab tile),
-//                                   z at the teacher entries, dZ'' = 2^(y - R)
-//              lse_merge         -> log Z and the row factor (g/tau) M 2^(R - log2 Z)
-//              dz_fix, dz_teacher -> fallback rows; teacher cells (Eq. 3) / factor
-//   forward only:  logits_lse (with z at the teacher entries), lse_merge
+//              logits_dz         -> (reference, sum-exp) partials per (token, vocab
+//                                   tile), z at the teacher entries, dZ'' = 2^(y - R)
+//              row_finish        -> log Z, the row factor (g/tau) M 2^(R - log2 Z),
+//                                   fallback rows, teacher cells (Eq. 3) / factor,
+//                                   l_t = H - C/tau + M log Z       (Eq. 2)
+//   forward only:  logits_lse (with z at the teacher entries), lse_merge, row_loss
 //   backward only: dz            -> recomputed logits, dZ = g/tau (M q - p)
-//              row_loss          -> l_t = H - C/tau + M log Z       (Eq. 2)
 //              dh (+ split reduce): dH = dZ W (per chunk or per group; rows scaled
 //                                   by the factor in the one-projection schedule)
 // Per group of chunks: transpose_rows, dw -> grad_W (+)= dZ^T H (fp32 accumulate)
@@ -591,8 +591,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
 // Once log Z is merged, the row factor (g/tau) M 2^(R - log2 Z) turns dZ''
 // into (g/tau) M q; it is applied to the rows of dH and, through the
 // transposed hidden rows, to dW, so dZ'' is never rewritten, except the
-// teacher cells (k_dz_teacher writes (g/tau)(M q - p) / factor, Eq. 3) and the
-// rare rows where a tile's sum of 2^(y - R) exceeded 2^kRefGap (k_dz_fix).
+// teacher cells (k_row_finish writes (g/tau)(M q - p) / factor, Eq. 3) and the
+// rare rows where a tile's sum of 2^(y - R) exceeded 2^kRefGap (k_row_finish
+// rescales them).
 // The [c, V] buffer is the same transient chunk the recompute schedule holds;
 // nothing grows with N. Staging and teacher bookkeeping are those of k_dz.
 template <typename T>
