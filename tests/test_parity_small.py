@@ -194,7 +194,18 @@ def test_deterministic(gpu_lib, dtype):
         assert torch.equal(a[k], b[k]), k
 
 
-@pytest.mark.parametrize("chunk", [7, 64, 259, 300])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_several_dw_groups(gpu_lib, dtype):
+    """20000 tokens in chunks of 4096: dW gathers 4 chunks per contraction, so
+    there are two groups, the second a single short chunk (3616 rows); dH runs
+    per group with its vocabulary range split (a chunk alone has 16 tiles).
+    Every element against the oracle."""
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(20000, 64, 1000, 8, tdt, seed=17, ignore_frac=0.05)
+    _run_and_compare(gpu_lib, inp, 1.0, 4096, TOL[dtype])
+
+
+@pytest.mark.parametrize("chunk", [1, 7, 64, 259, 300])
 def test_chunk_invariance(gpu_lib, chunk):
     inp = _inputs(259, 64, 1500, 6, torch.float32, seed=13, ignore_frac=0.1)
     args = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
