@@ -483,6 +483,12 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
         const DmaStep<NPW> sb = db.prep(opb, bS(cb), wave, ks, ks < ks_end);
         const char* a = aS(na);
         const char* b = bS(nb);
+        // the second half runs at wave priority 1, the first half, the waits
+        // and the barrier at 0: a wave still in its second half is issued
+        // before its SIMD partner that has moved on (measured: projection
+        // 4.5% and dH 1.5% faster; priority in the first half, or in both,
+        // was slower)
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int q = 0; q < NP; ++q) {
           if (q % DS == 0) sb.one(q / DS);
@@ -491,6 +497,7 @@ __device__ __forceinline__ void gemm_tile(const OA& opa, const OB& opb, int ks_b
           __builtin_amdgcn_sched_barrier(0);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       ca = na;
       cb = nb;
     }
