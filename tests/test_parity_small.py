@@ -134,6 +134,17 @@ def test_reference_logit_fallback(gpu_lib, dtype, flag_every, top_z, V):
     _run_and_compare(gpu_lib, inp, 1.0, chunk, TOL[dtype])
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_small_temperature(gpu_lib, dtype):
+    """tau = 0.02 stretches y = z log2(e) / tau to a spread of ~16 (base 2) per
+    token on random inputs, so many tile rows sum past 2^40 against the
+    reference logit and take the fallback to their own max (no constructed
+    logits). Loss and gradients against the oracle."""
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(259, 128, 4133, 7, tdt, seed=23, ignore_frac=0.1)
+    _run_and_compare(gpu_lib, inp, 0.02, 100, TOL[dtype])
+
+
 def test_all_ignored(gpu_lib):
     inp = _inputs(200, 64, 600, 5, torch.float32, seed=9)
     inp["ignore"] = torch.ones(200, dtype=torch.uint8, device="cuda")
