@@ -102,7 +102,8 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  *   hidden        [N, D] dtype        student hidden states h (row t = token t)
  *   W             [V, D] dtype        output projection
  *   teacher_idx   [N, K] int32        support S_t: K distinct indices in [0, V)
- *                                     per row (not range-checked here; see
+ *                                     per row (not range-checked here
+ *                                     unless KD_DEBUG_CHECK=1; see
  *                                     kd_topk_kl_check_indices)
  *   teacher_logit [N, K] fp32         teacher logits of the support; the
  *                                     teacher distribution is their softmax
@@ -223,6 +224,12 @@ kd_status kd_topk_kl_bwd(const kd_problem* p,
  * index (the support S_t of §3.2 is a set). Synchronises `hip_stream`.
  * Returns KD_OK, KD_ERR_BAD_INDEX, or an argument/device error. Uses the
  * first bytes of `workspace` (same size rule as kd_topk_kl_fwd_bwd).
+ *
+ * Debug mode: with the environment variable KD_DEBUG_CHECK set to 1 when a
+ * call is made, kd_topk_kl_fwd_bwd, kd_topk_kl_fwd and kd_topk_kl_bwd run
+ * this check first (synchronising their stream, so the call is no longer
+ * asynchronous) and return KD_ERR_BAD_INDEX with nothing else enqueued and no
+ * output touched when it fails. Without it, indices are not checked.
  */
 kd_status kd_topk_kl_check_indices(const kd_problem* p,
                                    const int32_t* teacher_idx,

@@ -3,6 +3,7 @@
 // operation goes through the launchers of kd_kernels.hip.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -141,6 +142,12 @@ Plan make_plan(const kd_problem* p) {
 }
 
 inline bool aligned16(const void* q) { return ((uintptr_t)q & 15u) == 0; }
+
+// KD_DEBUG_CHECK=1: every entry point validates the teacher indices first.
+bool debug_index_check() {
+  const char* e = getenv("KD_DEBUG_CHECK");
+  return e != nullptr && e[0] == '1' && e[1] == '\0';
+}
 
 }  // namespace
 
@@ -348,6 +355,10 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p, const void* hidden, const void
   const Plan pl = make_plan(p);
   st = validate(p, c, pl);
   if (st != KD_OK) return st;
+  if (debug_index_check() && p->N > 0) {
+    st = kd_topk_kl_check_indices(p, teacher_idx, workspace, workspace_bytes, hip_stream);
+    if (st != KD_OK) return st;
+  }
   return enqueue(p, pl, c);
 }
 
@@ -365,6 +376,10 @@ kd_status kd_topk_kl_fwd(const kd_problem* p, const void* hidden, const void* W,
   const Plan pl = make_plan(p);
   st = validate(p, c, pl);
   if (st != KD_OK) return st;
+  if (debug_index_check() && p->N > 0) {
+    st = kd_topk_kl_check_indices(p, teacher_idx, workspace, workspace_bytes, hip_stream);
+    if (st != KD_OK) return st;
+  }
   return enqueue(p, pl, c);
 }
 
@@ -383,6 +398,10 @@ kd_status kd_topk_kl_bwd(const kd_problem* p, const void* hidden, const void* W,
   const Plan pl = make_plan(p);
   st = validate(p, c, pl);
   if (st != KD_OK) return st;
+  if (debug_index_check() && p->N > 0) {
+    st = kd_topk_kl_check_indices(p, teacher_idx, workspace, workspace_bytes, hip_stream);
+    if (st != KD_OK) return st;
+  }
   return enqueue(p, pl, c);
 }
 

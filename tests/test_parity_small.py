@@ -228,6 +228,36 @@ def test_chunk_invariance(gpu_lib, chunk):
     assert rel_max(to64(out["grad_W"]), to64(ref["grad_W"])) <= 1e-6
 
 
+def test_debug_index_check(gpu_lib, monkeypatch):
+    """KD_DEBUG_CHECK=1: the entry points check the indices first and return
+    KD_ERR_BAD_INDEX (raised by the binding) with no output touched; valid
+    indices give the same result as without the check."""
+    inp = _inputs(300, 64, 1000, 20, torch.float32, seed=15)
+    args = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+    ref = gpu_lib.fwd_bwd(*args, chunk=128)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("KD_DEBUG_CHECK", "1")
+    out = gpu_lib.fwd_bwd(*args, chunk=128)
+    torch.cuda.synchronize()
+    assert float(out["loss"]) == float(ref["loss"])
+    assert torch.equal(out["grad_W"], ref["grad_W"])
+    for bad in (1000, -1):
+        idx = inp["teacher_idx"].clone()
+        idx[123, 4] = bad
+        for call in (lambda: gpu_lib.fwd_bwd(args[0], args[1], idx, args[3], chunk=128),
+                     lambda: gpu_lib.fwd(args[0], args[1], idx, args[3], chunk=128)):
+            with pytest.raises(gpu_lib.KdError) as e:
+                call()
+            assert e.value.code == 6
+    idx = inp["teacher_idx"].clone()
+    idx[7, 1] = idx[7, 0]  # a repeated index
+    f = gpu_lib.fwd(*args, chunk=128)
+    with pytest.raises(gpu_lib.KdError) as e:
+        gpu_lib.bwd(args[0], args[1], idx, args[3], f["saved_logz"], chunk=128)
+    assert e.value.code == 6
+    monkeypatch.delenv("KD_DEBUG_CHECK")
+
+
 def test_check_indices(gpu_lib):
     idx, _ = ki.make_teacher(300, 20, 1000, "cuda", seed=14)
     assert gpu_lib.check_indices(idx, V=1000)
