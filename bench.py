@@ -270,6 +270,43 @@ def split_schedule(inp, w, steps, ws, step_flops, peak):
             "mfma_pct_of_step": round(100.0 * step_flops / (ms / 1e3) / (peak * 1e12), 2)}
 
 
+def autograd_schedule(inp, w, steps):
+    """The step as a training loop takes it: topk_kl_loss(...).backward() with
+    hidden and W requiring gradients, for both autograd schedules (fused: one
+    kd_topk_kl_fwd_bwd call in the forward, the gradients scaled by the
+    upstream gradient in the backward; recompute: the split entry points).
+    Includes the autograd overhead and grad_W's conversion to W's dtype."""
+    import torch
+    import paper_2608_03796_amd as kd
+    h = inp["hidden"].detach().clone().requires_grad_(True)
+    Wp = inp["W"].detach().clone().requires_grad_(True)
+    res = {}
+    for sched in ("fused", "recompute"):
+        def step():
+            h.grad = None
+            Wp.grad = None
+            loss = kd.topk_kl_loss(h, Wp, inp["teacher_idx"], inp["teacher_logit"], tau=w.tau,
+                                   ignore=inp["ignore"], chunk=w.chunk, schedule=sched)
+            loss.backward()
+
+        step()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        print(f"bench: autograd {sched} {ms:.3f} ms/step", file=sys.stderr, flush=True)
+        res[sched] = {"ms_per_step": round(ms, 4), "tokens_per_s": round(w.N / (ms / 1e3), 1)}
+    del h, Wp
+    torch.cuda.empty_cache()
+    return {"call": "topk_kl_loss(...).backward(), hidden and W requiring gradients",
+            "steps": steps, **res}
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -390,6 +427,7 @@ def main():
     rec["mfma_pct_executed"] = round(100.0 * executed / (ms / 1e3) / (peak * 1e12), 2)
     if args.split_steps > 0:
         rec["recompute_schedule"] = split_schedule(inp, w, args.split_steps, ws, step_flops, peak)
+        rec["autograd"] = autograd_schedule(inp, w, args.split_steps)
     if args.cpu_rows > 0:
         print("bench: timing the CPU oracle baseline", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(inp, w, args.cpu_rows)

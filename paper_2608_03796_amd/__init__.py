@@ -300,15 +300,15 @@ def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ign
     return res
 
 
-def _autograd_function():
+def _autograd_functions():
     import torch
 
     class TopKKLLoss(torch.autograd.Function):
-        """Mean top-K KL loss as an autograd function: forward runs
-        kd_topk_kl_fwd and saves log Z; backward runs kd_topk_kl_bwd with the
-        upstream gradient. grad_W is returned in W's dtype (fp32 accumulation
-        inside one call; use bwd(..., accumulate_grad_W=True) to accumulate
-        micro-batches in fp32)."""
+        """Mean top-K KL loss as an autograd function, Algorithm 1's schedule:
+        forward runs kd_topk_kl_fwd and saves log Z; backward runs
+        kd_topk_kl_bwd with the upstream gradient (logit recompute). grad_W is
+        returned in W's dtype (fp32 accumulation inside one call; use
+        bwd(..., accumulate_grad_W=True) to accumulate micro-batches in fp32)."""
 
         @staticmethod
         def forward(ctx, hidden, W, teacher_idx, teacher_logit, tau, ignore, chunk,
@@ -335,20 +335,73 @@ def _autograd_function():
                 gW = gW.to(W.dtype)
             return res.get("grad_hidden"), gW, None, None, None, None, None, None
 
-    return TopKKLLoss
+    class TopKKLLossFused(torch.autograd.Function):
+        """Mean top-K KL loss as an autograd function, one projection per chunk:
+        when a gradient is wanted, forward runs kd_topk_kl_fwd_bwd and keeps the
+        gradients of the mean; backward multiplies them by the upstream
+        gradient (exact: the loss is linear in it). The gradients are held from
+        forward to backward; backward runs once per graph."""
+
+        @staticmethod
+        def forward(ctx, hidden, W, teacher_idx, teacher_logit, tau, ignore, chunk,
+                    teacher_logprobs):
+            need_h, need_W = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
+            ctx.grads = None
+            if not (need_h or need_W):
+                return fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
+                           chunk=chunk, teacher_logprobs=teacher_logprobs)["loss"]
+            out = fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
+                          chunk=chunk, grad_hidden=need_h, grad_W=need_W,
+                          teacher_logprobs=teacher_logprobs)
+            ctx.grads = [out.get("grad_hidden"), out.get("grad_W")]
+            ctx.w_dtype = W.dtype
+            return out["loss"]
+
+        @staticmethod
+        def backward(ctx, grad_out):
+            if ctx.grads is None:
+                raise RuntimeError("topk_kl_loss(schedule='fused') supports one backward per "
+                                   "graph; use schedule='recompute' to run backward again")
+            gh, gW = ctx.grads
+            ctx.grads = None
+            g = grad_out.detach().to(torch.float32)
+            if gh is not None:
+                gh = gh.mul_(g) if gh.dtype == torch.float32 else (gh.float() * g).to(gh.dtype)
+            if gW is not None:
+                gW = gW.mul_(g)
+                if gW.dtype != ctx.w_dtype:
+                    gW = gW.to(ctx.w_dtype)
+            return gh, gW, None, None, None, None, None, None
+
+    return {"recompute": TopKKLLoss, "fused": TopKKLLossFused}
 
 
 _TOPK_KL = None
 
 
 def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
-                 chunk: int = 4096, teacher_logprobs: bool = False):
-    """Differentiable mean top-K KL loss (autograd through the split entry points)."""
+                 chunk: int = 4096, teacher_logprobs: bool = False, schedule: str = "fused"):
+    """Differentiable mean top-K KL loss.
+
+    schedule="fused": when hidden or W needs a gradient, the forward computes
+    the loss and the gradients of the mean in one kd_topk_kl_fwd_bwd call (one
+    projection per chunk) and the backward scales them by the upstream
+    gradient; the gradients ([N, D] and the fp32 [V, D]) are held from forward
+    to backward, and backward runs once per graph.
+    schedule="recompute": Algorithm 1's schedule through the split entry
+    points (forward saves log Z; backward recomputes the logits)."""
+    import torch
     global _TOPK_KL
+    if schedule not in ("fused", "recompute"):
+        raise ValueError("schedule must be 'fused' or 'recompute'")
+    if not torch.is_grad_enabled():
+        # no graph will be built: the loss alone (no gradient work)
+        return fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore, chunk=chunk,
+                   teacher_logprobs=teacher_logprobs)["loss"]
     if _TOPK_KL is None:
-        _TOPK_KL = _autograd_function()
-    return _TOPK_KL.apply(hidden, W, teacher_idx, teacher_logit, float(tau), ignore, int(chunk),
-                          bool(teacher_logprobs))
+        _TOPK_KL = _autograd_functions()
+    return _TOPK_KL[schedule].apply(hidden, W, teacher_idx, teacher_logit, float(tau), ignore,
+                                    int(chunk), bool(teacher_logprobs))
 
 
 def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, workspace=None):

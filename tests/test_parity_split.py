@@ -144,7 +144,8 @@ def test_backward_accumulates_grad_W(gpu_lib):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_autograd_wrapper(gpu_lib, dtype):
+@pytest.mark.parametrize("schedule", ["fused", "recompute"])
+def test_autograd_wrapper(gpu_lib, dtype, schedule):
     kd = gpu_lib
     N, D, V, K, chunk, tau = 259, 128, 4133, 7, 100, 2.0
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
@@ -152,7 +153,7 @@ def test_autograd_wrapper(gpu_lib, dtype):
     h = inp["hidden"].clone().requires_grad_(True)
     W = inp["W"].clone().requires_grad_(True)
     loss = kd.topk_kl_loss(h, W, inp["teacher_idx"], inp["teacher_logit"], tau=tau,
-                           ignore=inp["ignore"], chunk=chunk)
+                           ignore=inp["ignore"], chunk=chunk, schedule=schedule)
     (3.0 * loss).backward()
     torch.cuda.synchronize()
     o = oracle_inputs(inp)
@@ -220,3 +221,32 @@ def test_forward_teacher_crowding_one_vocab_tile(gpu_lib, dtype):
     assert torch.equal(f["loss_per_token"], fb["loss_per_token"])
     ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk, want_grads=False)
     assert abs(float(f["loss"]) - ref["loss"]) <= TOL[dtype]["loss"] * abs(ref["loss"])
+
+
+def test_autograd_fused_schedule_cases(gpu_lib):
+    """The fused autograd schedule: a frozen W gets no gradient work and the
+    same hidden gradient; under no_grad only the loss is computed; a second
+    backward through the same graph is refused (the gradients are consumed);
+    the recompute schedule agrees."""
+    kd = gpu_lib
+    N, D, V, K, chunk = 200, 64, 1500, 6, 64
+    inp = _inputs(N, D, V, K, torch.float32, seed=12, ignore_frac=0.1)
+    idx, tl, ign = inp["teacher_idx"], inp["teacher_logit"], inp["ignore"]
+    h1 = inp["hidden"].clone().requires_grad_(True)
+    l1 = kd.topk_kl_loss(h1, inp["W"], idx, tl, ignore=ign, chunk=chunk)
+    (0.5 * l1).backward()
+    h2 = inp["hidden"].clone().requires_grad_(True)
+    l2 = kd.topk_kl_loss(h2, inp["W"], idx, tl, ignore=ign, chunk=chunk, schedule="recompute")
+    (0.5 * l2).backward()
+    torch.cuda.synchronize()
+    assert abs(float(l1) - float(l2)) <= 1e-6 * abs(float(l2))
+    assert rel_max(to64(h1.grad), to64(h2.grad)) <= 1e-5
+    with torch.no_grad():
+        l3 = kd.topk_kl_loss(inp["hidden"], inp["W"], idx, tl, ignore=ign, chunk=chunk)
+    assert l3.grad_fn is None
+    assert abs(float(l3) - float(l1)) <= 1e-6 * abs(float(l1))
+    h4 = inp["hidden"].clone().requires_grad_(True)
+    l4 = kd.topk_kl_loss(h4, inp["W"], idx, tl, ignore=ign, chunk=chunk)
+    l4.backward(retain_graph=True)
+    with pytest.raises(RuntimeError):
+        l4.backward()
