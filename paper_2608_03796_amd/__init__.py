@@ -366,11 +366,12 @@ def _autograd_functions():
             ctx.grads = None
             g = grad_out.detach().to(torch.float32)
             if gh is not None:
-                gh = gh.mul_(g) if gh.dtype == torch.float32 else (gh.float() * g).to(gh.dtype)
+                gh = gh.mul_(g)  # computed in fp32, rounded once to gh's dtype
             if gW is not None:
-                gW = gW.mul_(g)
-                if gW.dtype != ctx.w_dtype:
-                    gW = gW.to(ctx.w_dtype)
+                if ctx.w_dtype == torch.float32:
+                    gW = gW.mul_(g)
+                else:  # scaled and converted to W's dtype in one pass
+                    gW = torch.mul(gW, g, out=torch.empty_like(gW, dtype=ctx.w_dtype))
             return gh, gW, None, None, None, None, None, None
 
     return {"recompute": TopKKLLoss, "fused": TopKKLLossFused}
