@@ -270,12 +270,13 @@ def split_schedule(inp, w, steps, ws, step_flops, peak):
             "mfma_pct_of_step": round(100.0 * step_flops / (ms / 1e3) / (peak * 1e12), 2)}
 
 
-def autograd_schedule(inp, w, steps):
+def autograd_schedule(inp, w, steps, ws):
     """The step as a training loop takes it: topk_kl_loss(...).backward() with
     hidden and W requiring gradients, for both autograd schedules (fused: one
     kd_topk_kl_fwd_bwd call in the forward, the gradients scaled by the
     upstream gradient in the backward; recompute: the split entry points).
-    Includes the autograd overhead and grad_W's conversion to W's dtype."""
+    Includes the autograd overhead and grad_W's conversion to W's dtype; the
+    workspace is reused across calls, as a training loop would."""
     import torch
     import paper_2608_03796_amd as kd
     h = inp["hidden"].detach().clone().requires_grad_(True)
@@ -286,7 +287,8 @@ def autograd_schedule(inp, w, steps):
             h.grad = None
             Wp.grad = None
             loss = kd.topk_kl_loss(h, Wp, inp["teacher_idx"], inp["teacher_logit"], tau=w.tau,
-                                   ignore=inp["ignore"], chunk=w.chunk, schedule=sched)
+                                   ignore=inp["ignore"], chunk=w.chunk, schedule=sched,
+                                   workspace=ws)
             loss.backward()
 
         step()
@@ -427,7 +429,7 @@ def main():
     rec["mfma_pct_executed"] = round(100.0 * executed / (ms / 1e3) / (peak * 1e12), 2)
     if args.split_steps > 0:
         rec["recompute_schedule"] = split_schedule(inp, w, args.split_steps, ws, step_flops, peak)
-        rec["autograd"] = autograd_schedule(inp, w, args.split_steps)
+        rec["autograd"] = autograd_schedule(inp, w, args.split_steps, ws)
     if args.cpu_rows > 0:
         print("bench: timing the CPU oracle baseline", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline(inp, w, args.cpu_rows)

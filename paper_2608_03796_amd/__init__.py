@@ -312,12 +312,13 @@ def _autograd_functions():
 
         @staticmethod
         def forward(ctx, hidden, W, teacher_idx, teacher_logit, tau, ignore, chunk,
-                    teacher_logprobs):
+                    teacher_logprobs, workspace):
             res = fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore, chunk=chunk,
-                      teacher_logprobs=teacher_logprobs)
+                      teacher_logprobs=teacher_logprobs, workspace=workspace)
             ctx.save_for_backward(hidden, W, teacher_idx, teacher_logit, res["saved_logz"],
                                   *([ignore] if ignore is not None else []))
             ctx.cfg = (tau, chunk, teacher_logprobs, ignore is not None)
+            ctx.workspace = workspace
             return res["loss"]
 
         @staticmethod
@@ -329,11 +330,12 @@ def _autograd_functions():
             g = grad_out.detach().to(torch.float32).contiguous()
             need_h, need_W = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
             res = bwd(hidden, W, idx, tl, logz, tau=tau, ignore=ignore, chunk=chunk, grad_loss=g,
-                      grad_hidden=need_h, grad_W=need_W, teacher_logprobs=logprobs)
+                      grad_hidden=need_h, grad_W=need_W, teacher_logprobs=logprobs,
+                      workspace=ctx.workspace)
             gW = res.get("grad_W")
             if gW is not None and gW.dtype != W.dtype:
                 gW = gW.to(W.dtype)
-            return res.get("grad_hidden"), gW, None, None, None, None, None, None
+            return res.get("grad_hidden"), gW, None, None, None, None, None, None, None
 
     class TopKKLLossFused(torch.autograd.Function):
         """Mean top-K KL loss as an autograd function, one projection per chunk:
@@ -344,15 +346,16 @@ def _autograd_functions():
 
         @staticmethod
         def forward(ctx, hidden, W, teacher_idx, teacher_logit, tau, ignore, chunk,
-                    teacher_logprobs):
+                    teacher_logprobs, workspace):
             need_h, need_W = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
             ctx.grads = None
             if not (need_h or need_W):
                 return fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
-                           chunk=chunk, teacher_logprobs=teacher_logprobs)["loss"]
+                           chunk=chunk, teacher_logprobs=teacher_logprobs,
+                           workspace=workspace)["loss"]
             out = fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
                           chunk=chunk, grad_hidden=need_h, grad_W=need_W,
-                          teacher_logprobs=teacher_logprobs)
+                          teacher_logprobs=teacher_logprobs, workspace=workspace)
             ctx.grads = [out.get("grad_hidden"), out.get("grad_W")]
             ctx.w_dtype = W.dtype
             return out["loss"]
@@ -372,7 +375,7 @@ def _autograd_functions():
                     gW = gW.mul_(g)
                 else:  # scaled and converted to W's dtype in one pass
                     gW = torch.mul(gW, g, out=torch.empty_like(gW, dtype=ctx.w_dtype))
-            return gh, gW, None, None, None, None, None, None
+            return gh, gW, None, None, None, None, None, None, None
 
     return {"recompute": TopKKLLoss, "fused": TopKKLLossFused}
 
@@ -381,7 +384,8 @@ _TOPK_KL = None
 
 
 def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
-                 chunk: int = 4096, teacher_logprobs: bool = False, schedule: str = "fused"):
+                 chunk: int = 4096, teacher_logprobs: bool = False, schedule: str = "fused",
+                 workspace=None):
     """Differentiable mean top-K KL loss.
 
     schedule="fused": when hidden or W needs a gradient, the forward computes
@@ -390,7 +394,9 @@ def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore
     gradient; the gradients ([N, D] and the fp32 [V, D]) are held from forward
     to backward, and backward runs once per graph.
     schedule="recompute": Algorithm 1's schedule through the split entry
-    points (forward saves log Z; backward recomputes the logits)."""
+    points (forward saves log Z; backward recomputes the logits).
+    workspace: a uint8 device tensor of at least workspace_size(...) bytes to
+    reuse across calls (allocated per call when None)."""
     import torch
     global _TOPK_KL
     if schedule not in ("fused", "recompute"):
@@ -398,11 +404,11 @@ def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore
     if not torch.is_grad_enabled():
         # no graph will be built: the loss alone (no gradient work)
         return fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore, chunk=chunk,
-                   teacher_logprobs=teacher_logprobs)["loss"]
+                   teacher_logprobs=teacher_logprobs, workspace=workspace)["loss"]
     if _TOPK_KL is None:
         _TOPK_KL = _autograd_functions()
     return _TOPK_KL[schedule].apply(hidden, W, teacher_idx, teacher_logit, float(tau), ignore,
-                                    int(chunk), bool(teacher_logprobs))
+                                    int(chunk), bool(teacher_logprobs), workspace)
 
 
 def check_indices(teacher_idx, V, chunk=4096, D=64, tau=1.0, dtype=KD_BF16, workspace=None):

@@ -246,7 +246,10 @@ def test_autograd_fused_schedule_cases(gpu_lib):
     assert l3.grad_fn is None
     assert abs(float(l3) - float(l1)) <= 1e-6 * abs(float(l1))
     h4 = inp["hidden"].clone().requires_grad_(True)
-    l4 = kd.topk_kl_loss(h4, inp["W"], idx, tl, ignore=ign, chunk=chunk)
+    ws = kd.alloc_workspace(N, D, V, K, chunk, 1.0, kd.KD_F32, h4.device)
+    l4 = kd.topk_kl_loss(h4, inp["W"], idx, tl, ignore=ign, chunk=chunk, workspace=ws)
     l4.backward(retain_graph=True)
+    torch.cuda.synchronize()
+    assert rel_max(to64(h4.grad), to64(2.0 * h1.grad)) <= 1e-5
     with pytest.raises(RuntimeError):
         l4.backward()
