@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KDTOPK_ABI_VERSION 2
+#define KDTOPK_ABI_VERSION 3
 
 typedef enum kd_status {
   KD_OK = 0,
@@ -69,7 +69,7 @@ typedef struct kd_problem {
   int32_t K;           /* cached teacher entries per token; 1 <= K <= V, K <= 4096 */
   int32_t dtype;       /* kd_dtype of hidden, W and grad_hidden              */
   float temperature;   /* tau; finite and > 0                                */
-  int32_t flags;       /* 0 or KD_FLAG_TEACHER_LOGPROBS                      */
+  int32_t flags;       /* 0 or KD_FLAG_TEACHER_LOGPROBS | KD_FLAG_GRAD_HIDDEN_F32 */
 } kd_problem;
 
 /*
@@ -83,6 +83,14 @@ typedef struct kd_problem {
  * and sum_k exp(value) <= 1; this is not checked.
  */
 #define KD_FLAG_TEACHER_LOGPROBS 1
+
+/*
+ * KD_FLAG_GRAD_HIDDEN_F32: grad_hidden is written as fp32 whatever the
+ * problem's dtype (kd_topk_kl_fwd_bwd and kd_topk_kl_bwd), so that a caller
+ * who scales it later (kd_scale_grads) rounds to the hidden dtype only once.
+ * The pointer's buffer is then [N, D] fp32.
+ */
+#define KD_FLAG_GRAD_HIDDEN_F32 2
 
 /*
  * Bytes of device workspace kd_topk_kl_fwd_bwd, kd_topk_kl_fwd,
@@ -115,7 +123,9 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  *   loss          [1] fp32            out: mean of l_t over non-ignored
  *                                     tokens (0 if there are none)
  *   loss_per_token [N] fp32 or NULL   out: l_t (0 on ignored tokens)
- *   grad_hidden   [N, D] dtype or NULL  out: dL/dh; NULL skips its GEMMs
+ *   grad_hidden   [N, D] dtype or NULL  out: dL/dh (fp32 with
+ *                                     KD_FLAG_GRAD_HIDDEN_F32); NULL skips
+ *                                     its GEMMs
  *   grad_W        [V, D] fp32 or NULL   out: dL/dW; NULL skips its GEMMs
  *   accumulate_grad_W  0: grad_W = dL/dW;  1: grad_W += dL/dW (micro-batch
  *                                     accumulation)
@@ -196,7 +206,8 @@ kd_status kd_topk_kl_fwd(const kd_problem* p,
  *                                     per-token losses; when given, G uses
  *                                     g_t = u_t (ignored tokens 0) instead of
  *                                     grad_loss / N_valid
- *   grad_hidden   [N, D] dtype or NULL, grad_W [V, D] fp32 or NULL,
+ *   grad_hidden   [N, D] dtype (fp32 with KD_FLAG_GRAD_HIDDEN_F32) or NULL,
+ *   grad_W        [V, D] fp32 or NULL,
  *   accumulate_grad_W                 as for kd_topk_kl_fwd_bwd
  *
  * With grad_loss = NULL and no per-token gradients the results equal
@@ -236,6 +247,42 @@ kd_status kd_topk_kl_check_indices(const kd_problem* p,
                                    void* workspace,
                                    size_t workspace_bytes,
                                    void* hip_stream);
+
+/*
+ * Scales the gradients of the mean loss by the upstream gradient g of that
+ * mean, a device fp32 scalar: Algorithm 1's backward forms G = (M g) q - p g
+ * (§3.2.3); the loss is linear in g, so the gradients kd_topk_kl_fwd_bwd
+ * computed with g = 1 become those for any g by one multiplication. For a
+ * caller (an autograd function) that runs the fused call in its forward,
+ * before g is known: with KD_FLAG_GRAD_HIDDEN_F32 both gradients come out of
+ * the fused call in fp32, and each is rounded once, here, to its dtype.
+ *
+ *   grad_loss        [1] fp32                g (device)
+ *   grad_hidden_f32  [n_hidden] fp32 or NULL  input: dL/dh of the mean
+ *   grad_hidden_out  [n_hidden] hidden_dtype or NULL   out: g * input
+ *   grad_W_f32       [n_W] fp32 or NULL       input: dL/dW of the mean
+ *   grad_W_out       [n_W] w_dtype or NULL    out: g * input
+ *   hip_stream                                hipStream_t or NULL
+ *
+ * Each output is rounded once to its dtype (KD_F32 or KD_BF16). An fp32
+ * output may be its input itself (in place); otherwise output and input must
+ * not overlap. A NULL pair (or a zero count) skips that gradient.
+ * Asynchronous on hip_stream. Errors, all detected before any launch:
+ * KD_ERR_NULL_PTR (grad_loss NULL, or one of a pair NULL), KD_ERR_BAD_SHAPE
+ * (a negative count), KD_ERR_UNSUPPORTED (an output dtype other than KD_F32
+ * or KD_BF16, or a pointer not 16-byte aligned), KD_ERR_BAD_ARG (an output
+ * overlapping its input other than in place); KD_ERR_DEVICE (launch).
+ */
+kd_status kd_scale_grads(const float* grad_loss,
+                         const float* grad_hidden_f32,
+                         int32_t hidden_dtype,
+                         void* grad_hidden_out,
+                         int64_t n_hidden,
+                         const float* grad_W_f32,
+                         int32_t w_dtype,
+                         void* grad_W_out,
+                         int64_t n_W,
+                         void* hip_stream);
 
 /*
  * Instrumentation, not part of the method: per-kernel timing with HIP events.

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libkdtopk.so")
 KD_F32 = 0
 KD_BF16 = 1
 KD_FLAG_TEACHER_LOGPROBS = 1
+KD_FLAG_GRAD_HIDDEN_F32 = 2
 
 STATUS = {
     0: "KD_OK", 1: "KD_ERR_NULL_PTR", 2: "KD_ERR_BAD_SHAPE", 3: "KD_ERR_BAD_ARG",
@@ -24,8 +25,8 @@ STATUS = {
     7: "KD_ERR_DEVICE",
 }
 EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_fwd",
-            "kd_topk_kl_bwd", "kd_topk_kl_check_indices", "kd_status_string", "kd_abi_version",
-            "kd_profile_enable", "kd_profile_read")
+            "kd_topk_kl_bwd", "kd_topk_kl_check_indices", "kd_scale_grads", "kd_status_string",
+            "kd_abi_version", "kd_profile_enable", "kd_profile_read")
 
 
 class KdError(RuntimeError):
@@ -71,6 +72,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.kd_topk_kl_bwd.restype = ctypes.c_int
     lib.kd_topk_kl_check_indices.argtypes = [ctypes.POINTER(KdProblem), vp, vp, sz, vp]
     lib.kd_topk_kl_check_indices.restype = ctypes.c_int
+    lib.kd_scale_grads.argtypes = [vp, vp, ctypes.c_int32, vp, i64, vp, ctypes.c_int32, vp, i64,
+                                   vp]
+    lib.kd_scale_grads.restype = ctypes.c_int
     lib.kd_status_string.argtypes = [ctypes.c_int]
     lib.kd_status_string.restype = ctypes.c_char_p
     lib.kd_abi_version.argtypes = []
@@ -86,6 +90,11 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
 
 def problem(N, D, V, K, chunk, tau, dtype, flags=0) -> KdProblem:
     return KdProblem(int(N), int(D), int(V), int(chunk), int(K), int(dtype), float(tau), int(flags))
+
+
+def _flags(teacher_logprobs=False, grad_hidden_f32=False) -> int:
+    return (KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0) | \
+        (KD_FLAG_GRAD_HIDDEN_F32 if grad_hidden_f32 else 0)
 
 
 def _dtype_code(t) -> int:
@@ -175,15 +184,17 @@ def _check_workspace(workspace, device):
 def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
             chunk: int = 4096, grad_hidden: bool = True, grad_W: bool = True,
             loss_per_token: bool = False, grad_W_out=None, accumulate_grad_W: bool = False,
-            workspace=None, out=None, teacher_logprobs: bool = False):
+            workspace=None, out=None, teacher_logprobs: bool = False,
+            grad_hidden_f32: bool = False):
     """One call of kd_topk_kl_fwd_bwd on the current stream.
 
     hidden [N, D] and W [V, D] (bf16 or fp32, same dtype), teacher_idx [N, K]
     int32, teacher_logit [N, K] fp32 (log-probabilities of a partial-mass
     teacher when teacher_logprobs), ignore [N] uint8 or None. Returns a dict
     with 'loss' (0-d fp32 tensor), and 'loss_per_token', 'grad_hidden',
-    'grad_W' when requested. `out` may carry preallocated output tensors
-    (keys as returned) to make repeated calls allocation-free.
+    'grad_W' when requested. grad_hidden is in hidden's dtype, or fp32 with
+    grad_hidden_f32. `out` may carry preallocated output tensors (keys as
+    returned) to make repeated calls allocation-free.
     """
     import torch
     lib = load_library()
@@ -194,8 +205,9 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
         out["loss"] = torch.empty((), dtype=torch.float32, device=dev)
     if loss_per_token and "loss_per_token" not in out:
         out["loss_per_token"] = torch.empty(N, dtype=torch.float32, device=dev)
+    gh_dtype = torch.float32 if grad_hidden_f32 else hidden.dtype
     if grad_hidden and "grad_hidden" not in out:
-        out["grad_hidden"] = torch.empty(N, D, dtype=hidden.dtype, device=dev)
+        out["grad_hidden"] = torch.empty(N, D, dtype=gh_dtype, device=dev)
     if grad_W:
         if grad_W_out is not None:
             out["grad_W"] = grad_W_out
@@ -205,10 +217,10 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
     if loss_per_token:
         _check_tensor("loss_per_token", out["loss_per_token"], (N,), torch.float32, dev)
     if grad_hidden:
-        _check_tensor("grad_hidden", out["grad_hidden"], (N, D), hidden.dtype, dev)
+        _check_tensor("grad_hidden", out["grad_hidden"], (N, D), gh_dtype, dev)
     if grad_W:
         _check_tensor("grad_W", out["grad_W"], (V, D), torch.float32, dev)
-    pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
+    pr = problem(N, D, V, K, chunk, tau, dt, _flags(teacher_logprobs, grad_hidden_f32))
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
     _check_workspace(workspace, dev)
@@ -245,7 +257,7 @@ def fwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
            "saved_logz": torch.empty(N, dtype=torch.float32, device=dev)}
     if loss_per_token:
         res["loss_per_token"] = torch.empty(N, dtype=torch.float32, device=dev)
-    pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
+    pr = problem(N, D, V, K, chunk, tau, dt, _flags(teacher_logprobs))
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
     _check_workspace(workspace, dev)
@@ -285,7 +297,7 @@ def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ign
         res["grad_W"] = grad_W_out if grad_W_out is not None else torch.empty(
             V, D, dtype=torch.float32, device=dev)
         _check_tensor("grad_W", res["grad_W"], (V, D), torch.float32, dev)
-    pr = problem(N, D, V, K, chunk, tau, dt, KD_FLAG_TEACHER_LOGPROBS if teacher_logprobs else 0)
+    pr = problem(N, D, V, K, chunk, tau, dt, _flags(teacher_logprobs))
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
     _check_workspace(workspace, dev)
@@ -298,6 +310,42 @@ def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ign
     if rc != 0:
         raise KdError(rc, "kd_topk_kl_bwd")
     return res
+
+
+def scale_grads(grad_loss, grad_hidden=None, grad_hidden_out=None, grad_W=None,
+                grad_W_out=None):
+    """kd_scale_grads on the current stream: out = grad_loss * in for the fp32
+    gradients grad_hidden and grad_W of the mean loss, each written to its
+    output (fp32 or bf16; an fp32 output may be its input). grad_loss is the
+    upstream gradient of the mean, a one-element fp32 device tensor."""
+    import torch
+    lib = load_library()
+    pairs = (("grad_hidden", grad_hidden, grad_hidden_out), ("grad_W", grad_W, grad_W_out))
+    dev = None
+    for name, x, y in pairs:
+        if (x is None) != (y is None):
+            raise ValueError(f"{name} and its output go together")
+        if x is not None:
+            dev = x.device if dev is None else dev
+            _check_tensor(name, x, tuple(x.shape), torch.float32, dev)
+            _check_tensor(name + "_out", y, tuple(x.shape), y.dtype, dev)
+    if dev is None:
+        return
+    if grad_loss.numel() != 1:
+        raise ValueError("grad_loss must hold one value")
+    _check_tensor("grad_loss", grad_loss, tuple(grad_loss.shape), torch.float32, dev)
+
+    def code(y):
+        return _dtype_code(y.dtype) if y is not None else KD_F32
+
+    with torch.cuda.device(dev):
+        rc = lib.kd_scale_grads(
+            _ptr(grad_loss), _ptr(grad_hidden), code(grad_hidden_out), _ptr(grad_hidden_out),
+            grad_hidden.numel() if grad_hidden is not None else 0,
+            _ptr(grad_W), code(grad_W_out), _ptr(grad_W_out),
+            grad_W.numel() if grad_W is not None else 0, _stream_handle(dev))
+    if rc != 0:
+        raise KdError(rc, "kd_scale_grads")
 
 
 def _autograd_functions():
@@ -340,9 +388,10 @@ def _autograd_functions():
     class TopKKLLossFused(torch.autograd.Function):
         """Mean top-K KL loss as an autograd function, one projection per chunk:
         when a gradient is wanted, forward runs kd_topk_kl_fwd_bwd and keeps the
-        gradients of the mean; backward multiplies them by the upstream
-        gradient (exact: the loss is linear in it). The gradients are held from
-        forward to backward; backward runs once per graph."""
+        gradients of the mean (both in fp32); backward has kd_scale_grads
+        multiply them by the upstream gradient (exact: the loss is linear in
+        it) and round them once to the inputs' dtypes. The gradients are held
+        from forward to backward; backward runs once per graph."""
 
         @staticmethod
         def forward(ctx, hidden, W, teacher_idx, teacher_logit, tau, ignore, chunk,
@@ -355,9 +404,10 @@ def _autograd_functions():
                            workspace=workspace)["loss"]
             out = fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
                           chunk=chunk, grad_hidden=need_h, grad_W=need_W,
-                          teacher_logprobs=teacher_logprobs, workspace=workspace)
+                          teacher_logprobs=teacher_logprobs, workspace=workspace,
+                          grad_hidden_f32=True)
             ctx.grads = [out.get("grad_hidden"), out.get("grad_W")]
-            ctx.w_dtype = W.dtype
+            ctx.dtypes = (hidden.dtype, W.dtype)
             return out["loss"]
 
         @staticmethod
@@ -367,15 +417,18 @@ def _autograd_functions():
                                    "graph; use schedule='recompute' to run backward again")
             gh, gW = ctx.grads
             ctx.grads = None
-            g = grad_out.detach().to(torch.float32)
+            h_dtype, w_dtype = ctx.dtypes
+            g = grad_out.detach().to(torch.float32).contiguous()
+            # both gradients are fp32 here: scaled by g in the library and
+            # rounded once to the inputs' dtypes (in place when fp32)
+            gh_out = None
             if gh is not None:
-                gh = gh.mul_(g)  # computed in fp32, rounded once to gh's dtype
+                gh_out = gh if h_dtype == torch.float32 else torch.empty_like(gh, dtype=h_dtype)
+            gW_out = None
             if gW is not None:
-                if ctx.w_dtype == torch.float32:
-                    gW = gW.mul_(g)
-                else:  # scaled and converted to W's dtype in one pass
-                    gW = torch.mul(gW, g, out=torch.empty_like(gW, dtype=ctx.w_dtype))
-            return gh, gW, None, None, None, None, None, None, None
+                gW_out = gW if w_dtype == torch.float32 else torch.empty_like(gW, dtype=w_dtype)
+            scale_grads(g, grad_hidden=gh, grad_hidden_out=gh_out, grad_W=gW, grad_W_out=gW_out)
+            return gh_out, gW_out, None, None, None, None, None, None, None
 
     return {"recompute": TopKKLLoss, "fused": TopKKLLossFused}
 

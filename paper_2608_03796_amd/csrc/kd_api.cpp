@@ -45,7 +45,7 @@ struct Plan {
 
 kd_status check_problem(const kd_problem* p) {
   if (p == nullptr) return KD_ERR_NULL_PTR;
-  if ((p->flags & ~KD_FLAG_TEACHER_LOGPROBS) != 0) return KD_ERR_BAD_ARG;
+  if ((p->flags & ~(KD_FLAG_TEACHER_LOGPROBS | KD_FLAG_GRAD_HIDDEN_F32)) != 0) return KD_ERR_BAD_ARG;
   if (p->dtype != KD_F32 && p->dtype != KD_BF16) return KD_ERR_UNSUPPORTED;
   if (p->N < 0 || p->N >= kMaxN) return KD_ERR_BAD_SHAPE;
   if (p->D < 64 || p->D > kMaxD) return KD_ERR_BAD_SHAPE;
@@ -305,7 +305,8 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       h.tokens = n;
       h.split = choose_dh_split(cdiv(n, kTile) * pl.td, pl.ksteps);
       h.partial = h.split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
-      h.gH = static_cast<char*>(c.grad_hidden) + r0 * pl.D * pl.eb;
+      h.gh_f32 = (p->flags & KD_FLAG_GRAD_HIDDEN_F32) ? 1 : 0;
+      h.gH = static_cast<char*>(c.grad_hidden) + r0 * pl.D * (h.gh_f32 ? 4 : pl.eb);
       h.rowscale = scaled ? fac + zrow : nullptr;
       return kd_launch_dh(&h, c.stream) == 0;
     };
@@ -418,6 +419,41 @@ kd_status kd_topk_kl_check_indices(const kd_problem* p, const int32_t* teacher_i
   if (kd_launch_check_indices(teacher_idx, p->N, p->K, p->V, flag, &host_flag, hip_stream) != 0)
     return KD_ERR_DEVICE;
   return host_flag ? KD_ERR_BAD_INDEX : KD_OK;
+}
+
+// Checks one gradient of kd_scale_grads: in [n] fp32 -> out [n] dtype.
+static kd_status scale_one(const float* g, const float* in, int32_t dtype, void* out, int64_t n,
+                    void* stream) {
+  if ((in == nullptr) != (out == nullptr)) return KD_ERR_NULL_PTR;
+  if (n < 0) return KD_ERR_BAD_SHAPE;
+  if (in == nullptr || n == 0) return KD_OK;
+  if (dtype != KD_F32 && dtype != KD_BF16) return KD_ERR_UNSUPPORTED;
+  if (!aligned16(in) || !aligned16(out)) return KD_ERR_UNSUPPORTED;
+  // fp32 output: in place or disjoint; bf16 output: disjoint from the input
+  const uintptr_t a0 = (uintptr_t)in, a1 = a0 + (uintptr_t)n * 4;
+  const uintptr_t b0 = (uintptr_t)out, b1 = b0 + (uintptr_t)n * (dtype == KD_F32 ? 4 : 2);
+  if (a0 < b1 && b0 < a1 && !(dtype == KD_F32 && a0 == b0)) return KD_ERR_BAD_ARG;
+  return KD_OK;
+}
+
+kd_status kd_scale_grads(const float* grad_loss, const float* grad_hidden_f32,
+                         int32_t hidden_dtype, void* grad_hidden_out, int64_t n_hidden,
+                         const float* grad_W_f32, int32_t w_dtype, void* grad_W_out, int64_t n_W,
+                         void* hip_stream) {
+  if (grad_loss == nullptr) return KD_ERR_NULL_PTR;
+  kd_status st = scale_one(grad_loss, grad_hidden_f32, hidden_dtype, grad_hidden_out, n_hidden,
+                           hip_stream);
+  if (st != KD_OK) return st;
+  st = scale_one(grad_loss, grad_W_f32, w_dtype, grad_W_out, n_W, hip_stream);
+  if (st != KD_OK) return st;
+  if (grad_hidden_f32 != nullptr && n_hidden > 0 &&
+      kd_launch_scale(hidden_dtype == KD_BF16, grad_hidden_f32, grad_hidden_out, n_hidden,
+                      grad_loss, hip_stream) != 0)
+    return KD_ERR_DEVICE;
+  if (grad_W_f32 != nullptr && n_W > 0 &&
+      kd_launch_scale(w_dtype == KD_BF16, grad_W_f32, grad_W_out, n_W, grad_loss, hip_stream) != 0)
+    return KD_ERR_DEVICE;
+  return KD_OK;
 }
 
 }  // extern "C"

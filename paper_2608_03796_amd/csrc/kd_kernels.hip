@@ -942,7 +942,8 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, int64_t ldz,
                                                     const T* __restrict__ W, int V, int rows,
                                                     int D, int TM, int TN, int ks_total,
-                                                    int split, T* gH, float* partial,
+                                                    int split, void* gH, int gh_f32,
+                                                    float* partial,
                                                     const float* __restrict__ rowscale) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   const int tiles = TM * TN;
@@ -984,9 +985,13 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
       for (int r = 0; r < 4; ++r) {
         const int t = m0 + acc_m(wm, i, lane, r);
         if (t < rows) {
-          if (split == 1)
-            gH[(int64_t)t * D + d] = (T)(acc.v[i][j][r] * sc[r]);
-          else
+          if (split == 1) {
+            const float v = acc.v[i][j][r] * sc[r];
+            if (gh_f32)
+              static_cast<float*>(gH)[(int64_t)t * D + d] = v;
+            else
+              static_cast<T*>(gH)[(int64_t)t * D + d] = (T)v;
+          } else
             partial[((int64_t)sidx * rows + t) * D + d] = acc.v[i][j][r];
         }
       }
@@ -996,13 +1001,17 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
 
 template <typename T>
 __global__ void k_dh_reduce(const float* partial, int split, int64_t n, int D,
-                            const float* __restrict__ rowscale, T* gH) {
+                            const float* __restrict__ rowscale, void* gH, int gh_f32) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (; i < n; i += stride) {
     float s = 0.f;
     for (int k = 0; k < split; ++k) s += partial[(int64_t)k * n + i];
-    gH[i] = (T)(rowscale ? s * rowscale[i / D] : s);
+    const float v = rowscale ? s * rowscale[i / D] : s;
+    if (gh_f32)
+      static_cast<float*>(gH)[i] = v;
+    else
+      static_cast<T*>(gH)[i] = (T)v;
   }
 }
 
@@ -1154,6 +1163,36 @@ __global__ void k_check_indices(const int32_t* idx, int64_t N, int K, int64_t V,
       if (row[k2] == v) bad |= 2;
   }
   if (bad) atomicOr(flag, bad);
+}
+
+
+// ------------------------------------------------- upstream-gradient scale --
+// y = g x elementwise, g a device scalar: the gradients of the mean loss
+// times the upstream gradient of that mean (Algorithm 1's backward scales G
+// by g; the loss is linear in g, so scaling the finished gradients is the
+// same function). fp32 in; out in fp32 or bf16 (one rounding); in place when
+// x and y are the same fp32 buffer. Each thread handles 8 elements, 16-byte
+// accesses where the 8 are in range (the buffers are 16-byte aligned).
+template <typename TO>
+__global__ void k_scale_f32(const float* x, TO* y, int64_t n, const float* __restrict__ g) {
+  const float s = g[0];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x * 8;
+  for (int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8; i < n; i += stride) {
+    if (i + 8 <= n) {
+      const f32x4_t a = *reinterpret_cast<const f32x4_t*>(x + i) * s;
+      const f32x4_t b = *reinterpret_cast<const f32x4_t*>(x + i + 4) * s;
+      if constexpr (sizeof(TO) == 2) {
+        *reinterpret_cast<u32x4_t*>(y + i) =
+            u32x4_t{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]),
+                    pack_bf16x2(b[2], b[3])};
+      } else {
+        *reinterpret_cast<f32x4_t*>(y + i) = a;
+        *reinterpret_cast<f32x4_t*>(y + i + 4) = b;
+      }
+    } else {
+      for (int64_t k = i; k < n; ++k) y[k] = (TO)(x[k] * s);
+    }
+  }
 }
 
 }  // namespace kd
@@ -1356,14 +1395,14 @@ static int launch_dh_impl(const KdDhArgs& a, hipStream_t s) {
     ProfScope ps_(P_DH, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
     hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.split), dim3(kThreads), 0, s,
                        static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.W), (int)a.V,
-                       rows, (int)a.D, TM, TN, ks, a.split, static_cast<T*>(a.gH), a.partial,
+                       rows, (int)a.D, TM, TN, ks, a.split, a.gH, a.gh_f32, a.partial,
                        a.rowscale);
   }
   if (a.split > 1) {
     const int64_t n = (int64_t)rows * a.D;
     ProfScope ps_(P_DH_REDUCE, 0.0, s);
     hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256), 0,
-                       s, a.partial, a.split, n, (int)a.D, a.rowscale, static_cast<T*>(a.gH));
+                       s, a.partial, a.split, n, (int)a.D, a.rowscale, a.gH, a.gh_f32);
   }
   return (int)hipGetLastError();
 }
@@ -1437,3 +1476,20 @@ extern "C" int kd_launch_check_indices(const int32_t* idx, int64_t N, int K, int
   if (e != hipSuccess) return (int)e;
   return (int)hipStreamSynchronize(s);
 }
+
+// y = g x for the gradients (see k_scale_f32): x fp32, y fp32 (out_bf16 = 0)
+// or bf16 (out_bf16 = 1)
+extern "C" int kd_launch_scale(int out_bf16, const float* x, void* y, int64_t n, const float* g,
+                               void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n <= 0) return 0;
+  const int64_t blocks = std::min<int64_t>((n + 2047) / 2048, 8192);
+  if (out_bf16)
+    hipLaunchKernelGGL(k_scale_f32<__bf16>, dim3((int)blocks), dim3(256), 0, s, x,
+                       static_cast<__bf16*>(y), n, g);
+  else
+    hipLaunchKernelGGL(k_scale_f32<float>, dim3((int)blocks), dim3(256), 0, s, x,
+                       static_cast<float*>(y), n, g);
+  return (int)hipGetLastError();
+}
+

@@ -69,6 +69,7 @@ struct KdDhArgs {
   int split;                // split of the vocabulary (K) range, >= 1
   float* partial;           // [split, tokens, D] when split > 1
   void* gH;                 // grad_hidden + the group's first row * D
+  int gh_f32;               // grad_hidden is fp32 (else the operands' dtype)
   const float* rowscale;    // [tokens] factor of each dZ row, or null (= 1)
 };
 
@@ -94,6 +95,8 @@ int kd_launch_dh(const KdDhArgs* a, void* stream);
 int kd_launch_dw(const KdDwArgs* a, void* stream);
 int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid, float* loss,
                        void* stream);
+int kd_launch_scale(int out_bf16, const float* x, void* y, int64_t n, const float* g,
+                    void* stream);
 int kd_launch_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag,
                             int* host_flag, void* stream);
 }

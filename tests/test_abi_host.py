@@ -74,7 +74,7 @@ def _ws(lib, pr):
     (dict(D=96), 4), (dict(V=0), 2), (dict(V=2 ** 20 + 1), 2), (dict(K=0), 2),
     (dict(K=4097), 2), (dict(V=65536, K=4097), 2), (dict(chunk=0), 3), (dict(chunk=-5), 3), (dict(tau=0.0), 3),
     (dict(tau=-1.0), 3), (dict(tau=float("inf")), 3), (dict(tau=float("nan")), 3),
-    (dict(dtype=2), 4), (dict(dtype=-1), 4), (dict(flags=2), 3), (dict(flags=-1), 3),
+    (dict(dtype=2), 4), (dict(dtype=-1), 4), (dict(flags=4), 3), (dict(flags=-1), 3),
 ])
 def test_workspace_size_rejects(lib, kw, code):
     rc, _ = _ws(lib, _prob(**kw))
@@ -128,7 +128,7 @@ def _call(lib, pr, hidden=FAKE, W=FAKE, idx=FAKE, logit=FAKE, ignore=None, loss=
 
 @pytest.mark.parametrize("kw,code", [
     (dict(N=-3), 2), (dict(D=100), 4), (dict(K=5000), 2), (dict(chunk=0), 3),
-    (dict(tau=0.0), 3), (dict(dtype=7), 4), (dict(flags=2), 3),
+    (dict(tau=0.0), 3), (dict(dtype=7), 4), (dict(flags=4), 3),
 ])
 def test_fwd_bwd_rejects_problem(lib, kw, code):
     assert _call(lib, _prob(**kw)) == code
@@ -199,7 +199,7 @@ def _bwd(lib, pr, hidden=FAKE, W=FAKE, idx=FAKE, logit=FAKE, ignore=None, logz=F
 
 @pytest.mark.parametrize("kw,code", [
     (dict(N=-3), 2), (dict(D=100), 4), (dict(K=5000), 2), (dict(chunk=0), 3),
-    (dict(tau=0.0), 3), (dict(dtype=7), 4), (dict(flags=2), 3),
+    (dict(tau=0.0), 3), (dict(dtype=7), 4), (dict(flags=4), 3),
 ])
 def test_split_rejects_problem(lib, kw, code):
     assert _fwd(lib, _prob(**kw)) == code
@@ -237,3 +237,36 @@ def test_split_workspace_too_small(lib):
 @pytest.mark.parametrize("acc", [2, -1])
 def test_bwd_bad_accumulate(lib, acc):
     assert _bwd(lib, _prob(), acc=acc) == 3
+
+
+def test_grad_hidden_f32_flag_accepted(lib):
+    for flags in (2, 3):
+        rc, n = _ws(lib, _prob(flags=flags))
+        assert rc == 0 and n > 0
+
+
+def _scale(lib, g=FAKE, hin=None, hdt=kd.KD_F32, hout=None, nh=0, win=None, wdt=kd.KD_F32,
+           wout=None, nw=0):
+    return lib.kd_scale_grads(g, hin, hdt, hout, nh, win, wdt, wout, nw, None)
+
+
+def test_scale_grads_rejects(lib):
+    """kd_scale_grads: every argument error is found before any launch (the
+    pointers below are never dereferenced)."""
+    A, B = FAKE, FAKE + (1 << 20)
+    assert _scale(lib, g=None, hin=A, hout=B, nh=8) == 1                  # no g
+    assert _scale(lib, hin=A, hout=None, nh=8) == 1                      # half a pair
+    assert _scale(lib, win=None, wout=B, nw=8) == 1
+    assert _scale(lib, hin=A, hout=B, nh=-1) == 2                        # negative count
+    assert _scale(lib, win=A, wout=B, nw=-8) == 2
+    assert _scale(lib, hin=A, hdt=2, hout=B, nh=8) == 4                  # output dtype
+    assert _scale(lib, win=A, wdt=-1, wout=B, nw=8) == 4
+    assert _scale(lib, hin=FAKE_MISALIGNED, hout=B, nh=8) == 4           # alignment
+    assert _scale(lib, win=A, wout=FAKE_MISALIGNED, nw=8) == 4
+    assert _scale(lib, win=A, wdt=kd.KD_BF16, wout=A, nw=64) == 3        # bf16 onto its input
+    assert _scale(lib, win=A, wout=A + 16, nw=64) == 3                   # partial overlap
+    assert _scale(lib, hin=A, hdt=kd.KD_BF16, hout=A + 64, nh=64) == 3
+    # nothing to do: no launch, KD_OK
+    assert _scale(lib) == 0
+    assert _scale(lib, hin=A, hout=B, nh=0, win=A, wout=B, nw=0) == 0
+

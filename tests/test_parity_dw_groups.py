@@ -1,0 +1,64 @@
+"""grad_W on the dW path the benchmark times, every element against the oracle.
+
+At the benchmark's vocabulary (V = 131072) and chunk (4096 tokens), the fused
+call gathers the dZ rows of 4 chunks (16384 tokens) before each grad_W
+contraction: the K-major dZ operand then spans 4 GiB (its buffer resource is
+re-based every K step), the transposed hidden rows have a pitch of 16384
+tokens, and every group after the first accumulates into grad_W (beta = 1).
+A small hidden size keeps the fp64 oracle to seconds while every one of those
+conditions holds exactly as in the timed run; the oracle is evaluated over all
+N rows (row blocks on a thread pool, summed for grad_W). Algorithm 1's
+backward (dW += G^T h per chunk) and Eq. 3 define the reference.
+
+  * N = 32768: two full groups (the loss32k token count and grouping);
+  * N = 20000: a full group and a short last group of 3616 tokens (one
+    partial chunk), with 5% of the tokens ignored.
+
+grad_W is compared element by element, and so are grad_hidden (all rows), the
+per-token losses and the loss.
+"""
+import numpy as np
+import pytest
+import torch
+
+import kd_inputs as ki
+from oracle import kd_topk_kl
+from tests.helpers import TOL, oracle_by_row_blocks, rel_max, to64
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+@pytest.mark.parametrize("N,D,ign", [(32768, 64, 0.0), (20000, 128, 0.05)])
+def test_grad_W_full_groups(gpu_lib, N, D, ign):
+    V, K, chunk, tau = 131072, 100, 4096, 1.0
+    print(f"[dw-groups] N={N} D={D} V={V} K={K} chunk={chunk} ignored={ign}", flush=True)
+    dev = "cuda"
+    hidden = ki.make_hidden(N, D, torch.bfloat16, dev)
+    W = ki.make_weight(V, D, torch.bfloat16, dev)
+    idx, logit = ki.make_teacher(N, K, V, dev)
+    ignore = None
+    if ign > 0:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(ki.SEED_MASK)
+        ignore = torch.zeros(N, dtype=torch.uint8)
+        ignore[torch.randperm(N, generator=g)[:int(ign * N)]] = 1
+        ignore = ignore.to(dev)
+    # the grouping this test is about: 4 chunks per dW contraction, a 4 GiB
+    # dZ buffer in the workspace
+    ws = gpu_lib.workspace_size(N, D, V, K, chunk, tau, gpu_lib.KD_BF16)
+    assert ws >= 16384 * V * 2
+    out = gpu_lib.fwd_bwd(hidden, W, idx, logit, tau=tau, ignore=ignore, chunk=chunk,
+                          loss_per_token=True)
+    torch.cuda.synchronize()
+    ref = oracle_by_row_blocks(kd_topk_kl, to64(hidden), to64(W), to64(idx), to64(logit), tau,
+                               ignore=to64(ignore))
+    e_l = abs(float(out["loss"]) - ref["loss"]) / abs(ref["loss"])
+    e_t = rel_max(to64(out["loss_per_token"]), ref["loss_per_token"])
+    e_h = rel_max(to64(out["grad_hidden"]), ref["grad_hidden"])
+    e_w = rel_max(to64(out["grad_W"]), ref["grad_W"])
+    print(f"[dw-groups] N={N}: loss rel {e_l:.2e}, l_t {e_t:.2e}, grad_hidden {e_h:.2e}, "
+          f"grad_W {e_w:.2e}", flush=True)
+    assert e_l <= TOL["bf16"]["loss"]
+    assert e_t <= TOL["bf16"]["loss"]
+    assert e_h <= TOL["bf16"]["grad"]
+    assert e_w <= TOL["bf16"]["grad"]

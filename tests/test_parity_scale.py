@@ -86,7 +86,7 @@ def test_sampled_rows_and_properties(gpu_lib, name):
     assert e_h <= TOL["bf16"]["grad"]
 
 
-@pytest.mark.parametrize("name", ["loss4k", "packed"])
+@pytest.mark.parametrize("name", ["loss4k", "loss32k", "packed", "long256k"])
 def test_grad_W_sub_batch(gpu_lib, name):
     """grad_W of a 512-token sub-batch, every element against the oracle."""
     w = ki.WORKLOADS[name]

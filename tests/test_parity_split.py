@@ -233,16 +233,31 @@ def test_autograd_fused_schedule_cases(gpu_lib):
     inp = _inputs(N, D, V, K, torch.float32, seed=12, ignore_frac=0.1)
     idx, tl, ign = inp["teacher_idx"], inp["teacher_logit"], inp["ignore"]
     h1 = inp["hidden"].clone().requires_grad_(True)
+    kd.profile_read()
+    kd.profile_enable(True)
     l1 = kd.topk_kl_loss(h1, inp["W"], idx, tl, ignore=ign, chunk=chunk)
     (0.5 * l1).backward()
+    torch.cuda.synchronize()
+    kd.profile_enable(False)
+    ran = kd.profile_read()
+    # W is frozen: the call ran the projection and dH, and no grad_W work
+    assert "logits_dz" in ran and "dh" in ran
+    assert "dw" not in ran and "transpose_rows" not in ran, ran
     h2 = inp["hidden"].clone().requires_grad_(True)
     l2 = kd.topk_kl_loss(h2, inp["W"], idx, tl, ignore=ign, chunk=chunk, schedule="recompute")
     (0.5 * l2).backward()
     torch.cuda.synchronize()
     assert abs(float(l1) - float(l2)) <= 1e-6 * abs(float(l2))
     assert rel_max(to64(h1.grad), to64(h2.grad)) <= 1e-5
+    kd.profile_enable(True)
     with torch.no_grad():
         l3 = kd.topk_kl_loss(inp["hidden"], inp["W"], idx, tl, ignore=ign, chunk=chunk)
+    torch.cuda.synchronize()
+    kd.profile_enable(False)
+    ran = kd.profile_read()
+    # no graph: the forward alone, no gradient contraction
+    assert "logits_lse" in ran
+    assert not ({"logits_dz", "dz", "dh", "dw", "transpose_rows"} & set(ran)), ran
     assert l3.grad_fn is None
     assert abs(float(l3) - float(l1)) <= 1e-6 * abs(float(l1))
     h4 = inp["hidden"].clone().requires_grad_(True)
@@ -253,3 +268,33 @@ def test_autograd_fused_schedule_cases(gpu_lib):
     assert rel_max(to64(h4.grad), to64(2.0 * h1.grad)) <= 1e-5
     with pytest.raises(RuntimeError):
         l4.backward()
+
+
+@pytest.mark.parametrize("n", [1, 7, 8, 4097, 100003])
+def test_scale_grads(gpu_lib, n):
+    """kd_scale_grads: out = g * in from fp32 gradients, fp32 output exact (one
+    fp32 multiply, in place too) and bf16 output rounded once to nearest even
+    (compared with torch's own fp32 -> bf16 conversion of the fp32 product),
+    on sizes with ragged tails of the 8-element vectors."""
+    kd = gpu_lib
+    g = torch.Generator(device="cpu")
+    g.manual_seed(ki.SEED_TEACHER + n)
+    x = (torch.randn(n, generator=g) * 1e-3).to("cuda")
+    x2 = (torch.randn(n, generator=g) * 1e-6).to("cuda")
+    gl = torch.tensor([-2.7182817], dtype=torch.float32, device="cuda")
+    ref = (x.cpu() * gl.cpu()).contiguous()
+    ref2 = (x2.cpu() * gl.cpu()).contiguous()
+    out_bf = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    inplace = x2.clone()
+    kd.scale_grads(gl, grad_hidden=x, grad_hidden_out=out_bf, grad_W=inplace,
+                   grad_W_out=inplace)
+    torch.cuda.synchronize()
+    assert torch.equal(inplace.cpu(), ref2)
+    assert torch.equal(out_bf.cpu(), ref.to(torch.bfloat16))
+    # fp32 into a separate buffer, bf16 from the W slot
+    out32 = torch.empty(n, dtype=torch.float32, device="cuda")
+    out_bf2 = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    kd.scale_grads(gl, grad_hidden=x, grad_hidden_out=out32, grad_W=x2, grad_W_out=out_bf2)
+    torch.cuda.synchronize()
+    assert torch.equal(out32.cpu(), ref)
+    assert torch.equal(out_bf2.cpu(), ref2.to(torch.bfloat16))
