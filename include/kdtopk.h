@@ -249,6 +249,46 @@ kd_status kd_topk_kl_check_indices(const kd_problem* p,
                                    void* hip_stream);
 
 /*
+ * kd_topk_kl_fwd_bwd for callers that cannot allocate device memory (code
+ * being captured into a HIP graph, tight serving loops, harnesses that forbid
+ * allocation): the same arguments without the workspace. The workspace is a
+ * static per-device array of KD_SCRATCH_BYTES inside the library, which each
+ * device the library runs on holds from the first use of the library on that
+ * device until the process ends; the call itself allocates nothing (no
+ * hipMalloc, no events, no allocating library routine) and only enqueues
+ * kernels on hip_stream. The caller still provides every output.
+ *
+ * The plan is kd_topk_kl_fwd_bwd's when its workspace fits the array: results
+ * are then bitwise identical to kd_topk_kl_fwd_bwd's. Otherwise fewer chunks'
+ * dZ rows are gathered per grad_W contraction (grad_W differs only in the fp32
+ * summation order); if one chunk's workspace does not fit (about
+ * chunk * V * (element size) bytes plus small terms), the call returns
+ * KD_ERR_WORKSPACE_TOO_SMALL before touching the device: use a smaller chunk.
+ *
+ * Every call on a device shares that device's array, and calls keep no state
+ * in it (nothing in it has to start at zero; each call writes what it reads).
+ * Calls that overlap in time on one device (two streams, two threads) race on
+ * the array and give wrong results: order them on one stream. With
+ * KD_DEBUG_CHECK=1 the index check synchronises the stream, as for the other
+ * entry points. Errors as for kd_topk_kl_fwd_bwd, plus KD_ERR_WORKSPACE_TOO_SMALL
+ * as above and KD_ERR_DEVICE if the array's address cannot be obtained.
+ */
+#define KD_SCRATCH_BYTES (256u << 20)
+
+kd_status kd_topk_kl_fwd_bwd_noalloc(const kd_problem* p,
+                                     const void* hidden,
+                                     const void* W,
+                                     const int32_t* teacher_idx,
+                                     const float* teacher_logit,
+                                     const uint8_t* ignore,
+                                     float* loss,
+                                     float* loss_per_token,
+                                     void* grad_hidden,
+                                     float* grad_W,
+                                     int accumulate_grad_W,
+                                     void* hip_stream);
+
+/*
  * Scales the gradients of the mean loss by the upstream gradient g of that
  * mean, a device fp32 scalar: Algorithm 1's backward forms G = (M g) q - p g
  * (§3.2.3); the loss is linear in g, so the gradients kd_topk_kl_fwd_bwd

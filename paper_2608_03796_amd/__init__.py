@@ -24,7 +24,8 @@ STATUS = {
     4: "KD_ERR_UNSUPPORTED", 5: "KD_ERR_WORKSPACE_TOO_SMALL", 6: "KD_ERR_BAD_INDEX",
     7: "KD_ERR_DEVICE",
 }
-EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_fwd",
+EXPORTED = ("kd_topk_kl_workspace_size", "kd_topk_kl_fwd_bwd", "kd_topk_kl_fwd_bwd_noalloc",
+            "kd_topk_kl_fwd",
             "kd_topk_kl_bwd", "kd_topk_kl_check_indices", "kd_scale_grads", "kd_status_string",
             "kd_abi_version", "kd_profile_enable", "kd_profile_read")
 
@@ -64,6 +65,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.kd_topk_kl_fwd_bwd.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp, vp, vp, vp,
                                        vp, ctypes.c_int, vp, sz, vp]
     lib.kd_topk_kl_fwd_bwd.restype = ctypes.c_int
+    lib.kd_topk_kl_fwd_bwd_noalloc.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp,
+                                               vp, vp, vp, vp, ctypes.c_int, vp]
+    lib.kd_topk_kl_fwd_bwd_noalloc.restype = ctypes.c_int
     lib.kd_topk_kl_fwd.argtypes = [ctypes.POINTER(KdProblem), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    sz, vp]
     lib.kd_topk_kl_fwd.restype = ctypes.c_int
@@ -241,6 +245,44 @@ def fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None
     if grad_W:
         res["grad_W"] = out["grad_W"]
     return res
+
+
+def fwd_bwd_noalloc(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
+                    chunk: int = 4096, out=None, grad_hidden: bool = True, grad_W: bool = True,
+                    loss_per_token: bool = False, accumulate_grad_W: bool = False,
+                    teacher_logprobs: bool = False):
+    """kd_topk_kl_fwd_bwd_noalloc: kd_topk_kl_fwd_bwd with the library's own
+    static per-device scratch as workspace. Pass every wanted output in `out`
+    ('loss' 0-d fp32, 'loss_per_token' [N] fp32, 'grad_hidden' [N, D] in
+    hidden's dtype, 'grad_W' [V, D] fp32) to make the call allocation-free;
+    missing ones are allocated here. Returns the outputs as fwd_bwd does."""
+    import torch
+    lib = load_library()
+    N, D, V, K, dt = _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore)
+    dev = hidden.device
+    out = dict(out or {})
+    want = {"loss": ((), torch.float32, True),
+            "loss_per_token": ((N,), torch.float32, loss_per_token),
+            "grad_hidden": ((N, D), hidden.dtype, grad_hidden),
+            "grad_W": ((V, D), torch.float32, grad_W)}
+    for k, (shape, dtype, on) in want.items():
+        if not on:
+            continue
+        if k not in out:
+            out[k] = torch.empty(shape, dtype=dtype, device=dev)
+        _check_tensor(k, out[k], shape, dtype, dev)
+    pr = problem(N, D, V, K, chunk, tau, dt, _flags(teacher_logprobs))
+    with torch.cuda.device(dev):
+        rc = lib.kd_topk_kl_fwd_bwd_noalloc(
+            ctypes.byref(pr), _ptr(hidden), _ptr(W), _ptr(teacher_idx), _ptr(teacher_logit),
+            _ptr(ignore), _ptr(out["loss"]),
+            _ptr(out["loss_per_token"] if loss_per_token else None),
+            _ptr(out["grad_hidden"] if grad_hidden else None),
+            _ptr(out["grad_W"] if grad_W else None), int(bool(accumulate_grad_W)),
+            _stream_handle(dev))
+    if rc != 0:
+        raise KdError(rc, "kd_topk_kl_fwd_bwd_noalloc")
+    return {k: out[k] for k, (_, _, on) in want.items() if on}
 
 
 def fwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,

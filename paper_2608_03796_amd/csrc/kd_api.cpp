@@ -11,6 +11,8 @@
 #include "../../include/kdtopk.h"
 #include "kd_launch.h"
 
+static_assert(KD_SCRATCH_BYTES == kd_scratch_bytes_max, "scratch size in the header");
+
 namespace {
 
 constexpr int64_t kTile = 256;
@@ -73,7 +75,8 @@ int choose_dh_split(int64_t tiles, int64_t ksteps) {
   return best;
 }
 
-Plan make_plan(const kd_problem* p) {
+// g_max > 0 caps the chunks per dW group (see plan_within).
+Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
   Plan pl{};
   pl.N = p->N;
   pl.D = p->D;
@@ -92,6 +95,7 @@ Plan make_plan(const kd_problem* p) {
   pl.G = std::max<int64_t>(1, std::min<int64_t>(16384 / pl.c, std::max<int64_t>(pl.nchunks, 1)));
   pl.G = std::max<int64_t>(
       1, std::min<int64_t>(pl.G, ((int64_t)4 << 30) / std::max<int64_t>(pl.c * pl.Vp * pl.eb, 1)));
+  if (g_max > 0) pl.G = std::min<int64_t>(pl.G, g_max);
   // dH runs per chunk when a chunk's tiles fill the chip, else once per group
   // of G chunks (G times the tiles, dW's grouping); its vocabulary range is
   // split only when the rows it covers still have too few tiles
@@ -139,6 +143,17 @@ Plan make_plan(const kd_problem* p) {
   }
   pl.total = align256(t);
   return pl;
+}
+
+// The plan of make_plan, with fewer chunks per dW group if its workspace
+// exceeds `cap` bytes (the same plan when it fits); false if the workspace of
+// one chunk per group does not fit.
+bool plan_within(const kd_problem* p, size_t cap, Plan* out) {
+  Plan pl = make_plan(p);
+  while (pl.total > cap && pl.G > 1) pl = make_plan(p, pl.G - 1);
+  if (pl.total > cap) return false;
+  *out = pl;
+  return true;
 }
 
 inline bool aligned16(const void* q) { return ((uintptr_t)q & 15u) == 0; }
@@ -203,9 +218,10 @@ struct Call {
   void* stream;
 };
 
-// Common checks: problem, pointers every mode needs, alignment, workspace.
-kd_status validate(const kd_problem* p, const Call& c, const Plan& pl) {
-  if (c.ws == nullptr) return KD_ERR_NULL_PTR;
+// Common checks: problem, pointers every mode needs, alignment, workspace
+// (unless the workspace is the library's own scratch).
+kd_status validate(const kd_problem* p, const Call& c, const Plan& pl, bool own_ws = false) {
+  if (!own_ws && c.ws == nullptr) return KD_ERR_NULL_PTR;
   if (p->N > 0 && (c.hidden == nullptr || c.W == nullptr || c.idx == nullptr ||
                    c.tlogit == nullptr))
     return KD_ERR_NULL_PTR;
@@ -213,7 +229,7 @@ kd_status validate(const kd_problem* p, const Call& c, const Plan& pl) {
   if (!aligned16(c.hidden) || !aligned16(c.W) || !aligned16(c.grad_hidden) ||
       !aligned16(c.grad_W) || !aligned16(c.ws))
     return KD_ERR_UNSUPPORTED;
-  if (c.ws_bytes < pl.total) return KD_ERR_WORKSPACE_TOO_SMALL;
+  if (!own_ws && c.ws_bytes < pl.total) return KD_ERR_WORKSPACE_TOO_SMALL;
   return KD_OK;
 }
 
@@ -454,6 +470,39 @@ kd_status kd_scale_grads(const float* grad_loss, const float* grad_hidden_f32,
       kd_launch_scale(w_dtype == KD_BF16, grad_W_f32, grad_W_out, n_W, grad_loss, hip_stream) != 0)
     return KD_ERR_DEVICE;
   return KD_OK;
+}
+
+kd_status kd_topk_kl_fwd_bwd_noalloc(const kd_problem* p, const void* hidden, const void* W,
+                                     const int32_t* teacher_idx, const float* teacher_logit,
+                                     const uint8_t* ignore, float* loss, float* loss_per_token,
+                                     void* grad_hidden, float* grad_W, int accumulate_grad_W,
+                                     void* hip_stream) {
+  kd_status st = check_problem(p);
+  if (st != KD_OK) return st;
+  if (loss == nullptr) return KD_ERR_NULL_PTR;
+  Call c{KD_MODE_FWD_BWD, hidden, W, teacher_idx, teacher_logit, ignore, loss,
+         loss_per_token, nullptr, nullptr, nullptr, nullptr, grad_hidden, grad_W,
+         accumulate_grad_W, nullptr, 0, hip_stream};
+  Plan pl;
+  if (!plan_within(p, kd_scratch_bytes_max, &pl)) return KD_ERR_WORKSPACE_TOO_SMALL;
+  st = validate(p, c, pl, true);
+  if (st != KD_OK) return st;
+  // the device's scratch array (its address is looked up once per device)
+  void* ws = nullptr;
+  if (kd_scratch_get(&ws) != 0 || ws == nullptr) return KD_ERR_DEVICE;
+  c.ws = ws;
+  c.ws_bytes = kd_scratch_bytes_max;
+  if (debug_index_check() && p->N > 0) {
+    int* flag = reinterpret_cast<int*>(static_cast<char*>(ws) + pl.off_misc + 8);
+    int host_flag = 0;
+    if (kd_launch_check_indices(teacher_idx, p->N, p->K, p->V, flag, &host_flag, hip_stream) != 0)
+      return KD_ERR_DEVICE;
+    if (host_flag) return KD_ERR_BAD_INDEX;
+  }
+  kd_launch_suppress_profiling(1);
+  st = enqueue(p, pl, c);
+  kd_launch_suppress_profiling(0);
+  return st;
 }
 
 }  // extern "C"

@@ -1224,6 +1224,8 @@ struct ProfRec {
   double flops;
 };
 std::atomic<int> g_prof_mode{0};  // 0 off, 1 every kernel, 2 contractions only
+// set while the allocation-free entry point enqueues: no events are created
+thread_local bool t_prof_suppressed = false;
 std::mutex g_prof_mu;
 std::vector<ProfRec> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
@@ -1247,7 +1249,7 @@ struct ProfScope {
   hipEvent_t a = nullptr;
   ProfScope(int k, double f, hipStream_t st) : kind(k), flops(f), s(st) {
     const int mode = g_prof_mode.load(std::memory_order_relaxed);
-    if (mode == 0 || (mode == 2 && f == 0.0)) return;
+    if (mode == 0 || (mode == 2 && f == 0.0) || t_prof_suppressed) return;
     std::lock_guard<std::mutex> g(g_prof_mu);
     a = prof_event();
     if (a) (void)hipEventRecord(a, s);
@@ -1493,3 +1495,36 @@ extern "C" int kd_launch_scale(int out_bf16, const float* x, void* y, int64_t n,
   return (int)hipGetLastError();
 }
 
+// ------------------------------------------------------ static scratch ------
+// The workspace of the allocation-free entry point: one file-scope array per
+// device, held until the process ends. In host code the array's name denotes
+// a host-side stand-in, not device memory, so host code never uses it as an
+// address: the device address comes from hipGetSymbolAddress, once per
+// device with that device current, and only that address is passed to
+// kernels. Every call on a device shares its array.
+static __device__ __align__(256) char scratch[kd_scratch_bytes_max];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+}  // namespace
+
+extern "C" int kd_scratch_get(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  if (dev < 0 || dev >= kMaxDevices) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return (int)e;
+    if (p == nullptr) return (int)hipErrorInvalidSymbol;
+    g_scratch[dev] = p;
+  }
+  *ptr = g_scratch[dev];
+  return 0;
+}
+
+extern "C" void kd_launch_suppress_profiling(int on) { t_prof_suppressed = on != 0; }

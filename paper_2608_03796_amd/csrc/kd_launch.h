@@ -16,6 +16,9 @@ struct KdPrepareArgs {
 
 enum { KD_MODE_FWD_BWD = 0, KD_MODE_FWD = 1, KD_MODE_BWD = 2 };
 
+// bytes of the allocation-free entry point's static per-device scratch
+constexpr size_t kd_scratch_bytes_max = (size_t)256 << 20;
+
 // tokens per loss partial (one block of the row-loss kernels, a wave per token)
 constexpr int kLossRows = 4;
 
@@ -97,6 +100,10 @@ int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid, fl
                        void* stream);
 int kd_launch_scale(int out_bf16, const float* x, void* y, int64_t n, const float* g,
                     void* stream);
+// the current device's scratch address (hipGetSymbolAddress on first use)
+int kd_scratch_get(void** ptr);
+// nonzero: the calling thread's launches record no profiling events
+void kd_launch_suppress_profiling(int on);
 int kd_launch_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag,
                             int* host_flag, void* stream);
 }

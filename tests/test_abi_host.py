@@ -270,3 +270,24 @@ def test_scale_grads_rejects(lib):
     assert _scale(lib) == 0
     assert _scale(lib, hin=A, hout=B, nh=0, win=A, wout=B, nw=0) == 0
 
+
+def test_noalloc_rejects_before_the_device(lib):
+    """The allocation-free entry point refuses, on the host, a problem whose
+    one-chunk workspace exceeds the library's static scratch
+    (KD_ERR_WORKSPACE_TOO_SMALL), and every argument error of
+    kd_topk_kl_fwd_bwd, before it touches a device (none here)."""
+    v = lambda x: None if x is None else ctypes.c_void_p(x)
+
+    def call(pr, loss=FAKE, hidden=FAKE, acc=0):
+        return lib.kd_topk_kl_fwd_bwd_noalloc(ctypes.byref(pr), v(hidden), v(FAKE), v(FAKE),
+                                              v(FAKE), None, v(loss), None, v(FAKE), v(FAKE),
+                                              acc, None)
+    big = _prob(N=8192, D=4096, V=131072, K=100, chunk=4096, dtype=kd.KD_BF16)
+    assert call(big) == 5
+    assert call(_prob(chunk=0)) == 3
+    assert call(_prob(), loss=None) == 1
+    assert call(_prob(), hidden=None) == 1
+    assert call(_prob(), hidden=FAKE_MISALIGNED) == 4
+    assert call(_prob(), acc=2) == 3
+    assert lib.kd_topk_kl_fwd_bwd_noalloc(None, None, None, None, None, None, None, None, None,
+                                          None, 0, None) == 1

@@ -1,0 +1,73 @@
+"""The allocation-free entry point (kd_topk_kl_fwd_bwd_noalloc) against
+kd_topk_kl_fwd_bwd, through the C ABI, on consecutive calls that share the
+library's static scratch, each smaller than the one before:
+
+  1. bf16, N=2048, D=64, V=131072, chunk 512: kd_topk_kl_fwd_bwd's plan
+     (4 chunks per grad_W contraction, 512 MiB of dZ) does not fit the
+     256 MiB scratch, so one chunk per contraction is used: loss and per-token
+     losses are bitwise equal (the projections are the same), the gradients
+     equal within the fp32 summation order (bf16 bound of the contract);
+  2. bf16, N=1000, D=256, V=50000, chunk 256, tau 1.5, 10% ignored: the plan
+     fits, so every output is bitwise equal;
+  3. fp32, N=300, D=128, V=4133, K=7, chunk 100, tau 2, 20% ignored: bitwise.
+
+The stale contents each call leaves in the scratch must not leak into the next.
+"""
+import pytest
+import torch
+
+import kd_inputs as ki
+from tests.helpers import TOL, rel_max, to64
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # N, D, V, K, chunk, tau, ignored, dtype, plan unchanged
+    (2048, 64, 131072, 100, 512, 1.0, 0.0, torch.bfloat16, False),
+    (1000, 256, 50000, 32, 256, 1.5, 0.1, torch.bfloat16, True),
+    (300, 128, 4133, 7, 100, 2.0, 0.2, torch.float32, True),
+]
+
+
+def _inputs(N, D, V, K, dtype, ign, seed):
+    dev = "cuda"
+    hidden = ki.make_hidden(N, D, dtype, dev, seed=ki.SEED_HIDDEN + seed)
+    W = ki.make_weight(V, D, dtype, dev, seed=ki.SEED_W + seed)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + seed)
+    ignore = None
+    if ign > 0:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(ki.SEED_MASK + seed)
+        ignore = (torch.rand(N, generator=g) < ign).to(torch.uint8).to(dev)
+    return hidden, W, idx, logit, ignore
+
+
+def test_noalloc_matches_fwd_bwd(gpu_lib):
+    kd = gpu_lib
+    for n, (N, D, V, K, chunk, tau, ign, dtype, same_plan) in enumerate(CASES):
+        print(f"[noalloc] call {n + 1}: N={N} D={D} V={V} K={K} chunk={chunk} {dtype}",
+              flush=True)
+        hidden, W, idx, logit, ignore = _inputs(N, D, V, K, dtype, ign, seed=100 + n)
+        ref = kd.fwd_bwd(hidden, W, idx, logit, tau=tau, ignore=ignore, chunk=chunk,
+                         loss_per_token=True)
+        out = {"loss": torch.empty((), dtype=torch.float32, device="cuda"),
+               "loss_per_token": torch.full((N,), float("nan"), device="cuda"),
+               "grad_hidden": torch.full((N, D), float("nan"), dtype=dtype, device="cuda"),
+               "grad_W": torch.full((V, D), float("nan"), device="cuda")}
+        got = kd.fwd_bwd_noalloc(hidden, W, idx, logit, tau=tau, ignore=ignore, chunk=chunk,
+                                 out=out, loss_per_token=True)
+        torch.cuda.synchronize()
+        for k in ("loss", "loss_per_token", "grad_hidden", "grad_W"):
+            assert got[k].data_ptr() == out[k].data_ptr()
+        assert torch.equal(got["loss"], ref["loss"])
+        assert torch.equal(got["loss_per_token"], ref["loss_per_token"])
+        if same_plan:
+            assert torch.equal(got["grad_hidden"], ref["grad_hidden"])
+            assert torch.equal(got["grad_W"], ref["grad_W"])
+        else:
+            tol = TOL["bf16" if dtype == torch.bfloat16 else "f32"]["grad"]
+            e_h = rel_max(to64(got["grad_hidden"]), to64(ref["grad_hidden"]))
+            e_w = rel_max(to64(got["grad_W"]), to64(ref["grad_W"]))
+            print(f"[noalloc] call {n + 1}: capped plan, grad_hidden {e_h:.2e}, "
+                  f"grad_W {e_w:.2e}", flush=True)
+            assert e_h <= tol and e_w <= tol
