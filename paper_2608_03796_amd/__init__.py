@@ -486,8 +486,15 @@ def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore
     schedule="fused": when hidden or W needs a gradient, the forward computes
     the loss and the gradients of the mean in one kd_topk_kl_fwd_bwd call (one
     projection per chunk) and the backward scales them by the upstream
-    gradient; the gradients ([N, D] and the fp32 [V, D]) are held from forward
-    to backward, and backward runs once per graph.
+    gradient in the library (kd_scale_grads), rounding each once to its
+    input's dtype; backward runs once per graph. Cost when no backward
+    follows (a loss only logged with grad mode on): the forward still does
+    all the gradient work (about 3x the forward-only time) and holds the fp32
+    gradients ([N, D] and [V, D]: 2.5 GiB at N = 32768, D = 4096,
+    V = 131072) until the graph is freed; they are kept on the autograd
+    context, so saved-tensor hooks (offloading) do not see them. Compute such
+    a loss under torch.no_grad(), or use schedule="recompute", whose forward
+    is kd_topk_kl_fwd alone and which saves only log Z.
     schedule="recompute": Algorithm 1's schedule through the split entry
     points (forward saves log Z; backward recomputes the logits).
     workspace: a uint8 device tensor of at least workspace_size(...) bytes to

@@ -40,6 +40,8 @@ struct Plan {
   int64_t G;           // chunks whose dZ rows are gathered before one dH and one dW GEMM
   int64_t ngroups;
   bool dh_per_group;   // dH once per group (a chunk alone has too few tiles) or per chunk
+  bool prep_per_group; // rows prepared once per group (chunks of whole 256-token tiles)
+  int64_t ng;          // rows of the per-row arrays: the group's, or one chunk's (padded)
   int64_t td, ksteps;  // dH column tiles and K steps (for its vocabulary split)
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
       off_lossp, off_dz, off_fac, off_ht, off_dhs, total;
@@ -100,6 +102,11 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
   // of G chunks (G times the tiles, dW's grouping); its vocabulary range is
   // split only when the rows it covers still have too few tiles
   pl.ngroups = cdiv(pl.nchunks, pl.G);
+  // the teacher prologue, bucketing and reference logits run once per group
+  // when every chunk starts on a 256-token tile of the group (the buckets are
+  // per tile), else once per chunk
+  pl.prep_per_group = pl.G > 1 && pl.c % kTile == 0;
+  pl.ng = pl.prep_per_group ? pl.G * pl.c : pl.cp;
   pl.td = cdiv(pl.D, kTile);
   pl.ksteps = pl.Vp * pl.eb / 128;
   pl.dh_per_group = choose_dh_split(cdiv(pl.c, kTile) * pl.td, pl.ksteps) > 1;
@@ -118,14 +125,14 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
     return o;
   };
   pl.off_misc = take(256);
-  pl.off_p = take((size_t)pl.cp * pl.K * 4);
-  pl.off_rows = take((size_t)7 * pl.cp * 4);
+  pl.off_p = take((size_t)pl.ng * pl.K * 4);
+  pl.off_rows = take((size_t)7 * pl.ng * 4);
   pl.off_pm = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
-  pl.off_hits = take((size_t)pl.cp * pl.K * 4);
-  pl.off_hitp = take((size_t)pl.cp * pl.K * 4);
-  pl.off_hoff = take((size_t)(pl.cp / kTile) * (pl.nVT + 1) * 4);
-  pl.off_zhit = take((size_t)pl.cp * pl.K * 4);
+  pl.off_hits = take((size_t)pl.ng * pl.K * 4);
+  pl.off_hitp = take((size_t)pl.ng * pl.K * 4);
+  pl.off_hoff = take((size_t)(pl.ng / kTile) * (pl.nVT + 1) * 4);
+  pl.off_zhit = take((size_t)pl.ng * pl.K * 4);
   pl.off_lossp = take((size_t)std::max<int64_t>(pl.nchunks, 1) * pl.nblk * 4);
   pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
   // factor of each dZ row of the group in the single-projection schedule
@@ -262,12 +269,13 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
   int64_t n_partials = 0;
   int64_t group_tokens = 0;
   bool dw_done = false;
-  for (int64_t ci = 0; ci < pl.nchunks; ++ci) {
-    const int64_t row0 = ci * pl.c;
-    const int rcount = (int)std::min<int64_t>(pl.c, pl.N - row0);
+  // the per-row arrays from row `o` of the prepared rows
+  auto chunk_args = [&](int64_t row0, int rcount, int64_t o, int stages) {
     KdChunkArgs a{};
     a.dtype = p->dtype;
     a.mode = c.mode;
+    a.stages = stages;
+    a.one_projection = scaled ? 1 : 0;
     a.teacher_logprobs = (p->flags & KD_FLAG_TEACHER_LOGPROBS) ? 1 : 0;
     a.gscale = c.gscale;
     a.gtok = c.gtok;
@@ -285,22 +293,35 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.tlogit = c.tlogit;
     a.ignore = c.ignore;
     a.inv_nvalid = inv_nvalid;
-    a.p = reinterpret_cast<float*>(ws + pl.off_p);
-    a.rowM = rows;
-    a.rowH = rows + pl.cp;
-    a.rowCoef = rows + 2 * pl.cp;
-    a.rowCoefM = rows + 3 * pl.cp;
-    a.rowL2 = rows + 4 * pl.cp;
-    a.rowR = rows + 5 * pl.cp;
-    a.rowFlag = reinterpret_cast<int*>(rows + 6 * pl.cp);
+    a.p = reinterpret_cast<float*>(ws + pl.off_p) + o * pl.K;
+    a.rowM = rows + o;
+    a.rowH = rows + pl.ng + o;
+    a.rowCoef = rows + 2 * pl.ng + o;
+    a.rowCoefM = rows + 3 * pl.ng + o;
+    a.rowL2 = rows + 4 * pl.ng + o;
+    a.rowR = rows + 5 * pl.ng + o;
+    a.rowFlag = reinterpret_cast<int*>(rows + 6 * pl.ng) + o;
     a.part_m = reinterpret_cast<float*>(ws + pl.off_pm);
     a.part_s = reinterpret_cast<float*>(ws + pl.off_ps);
-    a.hits = reinterpret_cast<uint32_t*>(ws + pl.off_hits);
-    a.hitp = reinterpret_cast<float*>(ws + pl.off_hitp);
-    a.hoff = reinterpret_cast<int*>(ws + pl.off_hoff);
-    a.zhit = reinterpret_cast<float*>(ws + pl.off_zhit);
+    a.hits = reinterpret_cast<uint32_t*>(ws + pl.off_hits) + o * pl.K;
+    a.hitp = reinterpret_cast<float*>(ws + pl.off_hitp) + o * pl.K;
+    a.hoff = reinterpret_cast<int*>(ws + pl.off_hoff) + (o / kTile) * (pl.nVT + 1);
+    a.zhit = reinterpret_cast<float*>(ws + pl.off_zhit) + o * pl.K;
     a.nVT = (int)pl.nVT;
+    return a;
+  };
+  for (int64_t ci = 0; ci < pl.nchunks; ++ci) {
+    const int64_t row0 = ci * pl.c;
+    const int rcount = (int)std::min<int64_t>(pl.c, pl.N - row0);
     const int64_t slot = ci % pl.G;
+    if (pl.prep_per_group && slot == 0) {
+      const int grows = (int)std::min<int64_t>(pl.G * pl.c, pl.N - row0);
+      KdChunkArgs g = chunk_args(row0, grows, 0, KD_STAGE_PREP);
+      if (kd_launch_chunk(&g, c.stream) != 0) return KD_ERR_DEVICE;
+    }
+    KdChunkArgs a = chunk_args(row0, rcount, pl.prep_per_group ? slot * pl.c : 0,
+                               pl.prep_per_group ? KD_STAGE_CHUNK
+                                                 : (KD_STAGE_PREP | KD_STAGE_CHUNK));
     a.rowFactor = fac + slot * pl.c;
     a.dZ = (want_dh || want_dw) ? ws + pl.off_dz + slot * pl.c * pl.Vp * pl.eb : nullptr;
     a.ldz = pl.Vp;

@@ -1313,27 +1313,30 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
   const double gemm_flops = 2.0 * (double)a.rows * (double)a.D * (double)a.V;
 
   const bool fwd = a.mode != KD_MODE_BWD, bwd = a.mode != KD_MODE_FWD;
-{
-    ProfScope ps_(P_PROLOGUE, 0.0, s);
-    hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
-                     a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.teacher_logprobs, a.inv_nvalid,
-                     a.gscale, a.gtok, fwd ? nullptr : a.logz_in, a.p, a.rowM, a.rowH, a.rowCoef,
-                     a.rowCoefM, a.rowL2);
-    }
-{
-    ProfScope ps_(P_BUCKET, 0.0, s);
-    hipLaunchKernelGGL(k_bucket, dim3(TNt), dim3(kBucketThreads), 0, s, a.tidx, a.p, a.rows, a.K,
-                       (int)a.V, a.nVT, a.hits, a.hitp, a.hoff, a.zhit);
-    }
-  if (fwd && bwd && a.dZ != nullptr) {
-    // loss and gradients together: one projection per chunk (k_logits_dz)
-    // against the reference logit, then the merge of log Z with the row
-    // factors, the fallback rows, the teacher cells and the row losses
+  if (a.stages & KD_STAGE_PREP) {
     {
+      ProfScope ps_(P_PROLOGUE, 0.0, s);
+      hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
+                         a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.teacher_logprobs,
+                         a.inv_nvalid, a.gscale, a.gtok, fwd ? nullptr : a.logz_in, a.p, a.rowM,
+                         a.rowH, a.rowCoef, a.rowCoefM, a.rowL2);
+    }
+    {
+      ProfScope ps_(P_BUCKET, 0.0, s);
+      hipLaunchKernelGGL(k_bucket, dim3(TNt), dim3(kBucketThreads), 0, s, a.tidx, a.p, a.rows,
+                         a.K, (int)a.V, a.nVT, a.hits, a.hitp, a.hoff, a.zhit);
+    }
+    if (a.one_projection) {
       ProfScope ps_(P_REF, 0.0, s);
       hipLaunchKernelGGL(k_ref_logit<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, Hc, W, (int)a.D,
                          a.tidx, a.tlogit, a.row0, a.rows, a.K, (int)a.V, k2, a.rowR, a.rowFlag);
     }
+  }
+  if (!(a.stages & KD_STAGE_CHUNK)) return (int)hipGetLastError();
+  if (a.one_projection) {
+    // loss and gradients together: one projection per chunk (k_logits_dz)
+    // against the reference logit, then the merge of log Z with the row
+    // factors, the fallback rows, the teacher cells and the row losses
     {
       ProfScope ps_(P_LOGITS_DZ, gemm_flops, s);
       hipLaunchKernelGGL(k_logits_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,

@@ -22,9 +22,17 @@ constexpr size_t kd_scratch_bytes_max = (size_t)256 << 20;
 // tokens per loss partial (one block of the row-loss kernels, a wave per token)
 constexpr int kLossRows = 4;
 
+// Stages of kd_launch_chunk: preparing rows (teacher prologue, bucketing,
+// and in the one-projection schedule the reference logits) and the chunk's
+// projection and what follows it. The host prepares the rows of a whole dW
+// group at once when chunks align with 256-token tiles, else each chunk.
+enum { KD_STAGE_PREP = 1, KD_STAGE_CHUNK = 2 };
+
 struct KdChunkArgs {
   int dtype;
   int mode;                 // KD_MODE_*: which half of Algorithm 1 runs
+  int stages;               // KD_STAGE_* bits
+  int one_projection;       // loss and gradients together (k_logits_dz schedule)
   int teacher_logprobs;     // cached log-probabilities (partial mass) instead of logits
   const float* gscale;      // upstream gradient of the mean (device scalar) or null = 1
   const float* gtok;        // full [N] upstream per-token gradients or null
@@ -32,8 +40,8 @@ struct KdChunkArgs {
   float* logz_out;          // this chunk's rows of the saved log Z (forward) or null
   int64_t D, V;
   int K;
-  int64_t row0;             // first token of the chunk
-  int rows;                 // tokens in the chunk
+  int64_t row0;             // first token of the chunk (of the prepared rows)
+  int rows;                 // tokens in the chunk (prepared rows)
   float inv_tau;
   const void* W;            // [V, D]
   const void* Hc;           // hidden + row0 * D
