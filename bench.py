@@ -47,6 +47,10 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes three times (the "
                          "reference kernel that scales the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--blas-reference", action="store_true",
+                    help="only time the vendor GEMM (torch.matmul on hipBLASLt) on the "
+                         "workload's three contraction shapes in bf16, as a reference for the "
+                         "library's contraction kernels")
     ap.add_argument("--memory-sweep", action="store_true",
                     help="only measure peak allocated bytes of one fwd+bwd call at N = 4K..256K "
                          "(D=4096, V=131072, K=100, chunk 4096, bf16) and fit a + b N")
@@ -135,6 +139,55 @@ def memory_sweep():
                       "shapes": {"D": base.D, "V": base.V, "K": base.K, "chunk": base.chunk,
                                  "dtype": base.dtype},
                       "bf16_logits_at_262144_bytes": dense}), flush=True)
+
+
+def blas_reference(wname, reps=10):
+    """torch.matmul (hipBLASLt) on the contraction shapes of one chunk / dW group
+    of the workload, bf16 in and out, random operands of the workload's scales;
+    HIP-event time per call and the sampled shader clock. A plain GEMM: no
+    epilogue beyond the bf16 output write (the library's kernels add the
+    normaliser and dZ epilogue, a row scale, or grad_W's fp32 read-modify-write)."""
+    import torch
+    import kd_inputs as ki
+    w = ki.WORKLOADS[wname]
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(ki.SEED_HIDDEN)
+
+    def rn(*shape, std=1.0):
+        return (torch.randn(*shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    c = w.chunk
+    T = max(1, 16384 // c) * c  # tokens of one dW group
+    W = rn(w.V, w.D, std=0.02)
+    H = rn(c, w.D)
+    dZ = rn(c, w.V, std=1e-3)
+    Ht = rn(w.D, T)
+    dZg = rn(T, w.V, std=1e-3)
+    cases = [("projection z^T = W H_c^T", lambda: torch.matmul(W, H.t()), 2.0 * c * w.D * w.V),
+             ("dH = dZ W", lambda: torch.matmul(dZ, W), 2.0 * c * w.D * w.V),
+             ("dW^T = H^T dZ (one group)", lambda: torch.matmul(Ht, dZg), 2.0 * T * w.D * w.V)]
+    out = []
+    for name, f, fl in cases:
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        with ClockSampler(0.005) as ck:
+            e0.record()
+            for _ in range(reps):
+                f()
+            e1.record()
+            torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        clk = ck.mean()
+        out.append({"shape": name, "ms": round(ms, 4), "tflops": round(fl / ms / 1e9, 1),
+                    "sclk_mhz": round(clk, 1) if clk else None})
+        print(f"bench: blas {name}: {ms:.3f} ms, {fl / ms / 1e9:.0f} TFLOP/s", file=sys.stderr,
+              flush=True)
+    print(json.dumps({"blas_reference": out, "workload": wname,
+                      "torch": torch.__version__}), flush=True)
 
 
 def copy_calibration(nbytes):
@@ -343,6 +396,9 @@ def main():
         return
     if args.memory_sweep:
         memory_sweep()
+        return
+    if args.blas_reference:
+        blas_reference(args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: this build runs the loss on one "

@@ -38,13 +38,14 @@ struct Plan {
   int64_t nchunks;
   int64_t nblk;        // loss partials of a full chunk (one per kLossRows rows)
   int64_t G;           // chunks whose dZ rows are gathered before one dH and one dW GEMM
+  int64_t merged;      // caller's chunks per chunk of the plan (1 or the group size)
   int64_t ngroups;
   bool dh_per_group;   // dH once per group (a chunk alone has too few tiles) or per chunk
   bool prep_per_group; // rows prepared once per group (chunks of whole 256-token tiles)
   int64_t ng;          // rows of the per-row arrays: the group's, or one chunk's (padded)
   int64_t td, ksteps;  // dH column tiles and K steps (for its vocabulary split)
   size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
-      off_lossp, off_dz, off_fac, off_ht, off_dhs, total;
+      off_lossp, off_dz, off_fac, off_ht, off_dhs, off_dwp, total;
 };
 
 kd_status check_problem(const kd_problem* p) {
@@ -98,6 +99,27 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
   pl.G = std::max<int64_t>(
       1, std::min<int64_t>(pl.G, ((int64_t)4 << 30) / std::max<int64_t>(pl.c * pl.Vp * pl.eb, 1)));
   if (g_max > 0) pl.G = std::min<int64_t>(pl.G, g_max);
+  // Chunks of whole 256-token tiles that share a dW group are processed as one
+  // chunk of the group's rows when a chunk's projection leaves its last round
+  // of tiles partly filled (its tiles are not a multiple of the 256 compute
+  // units) and dH runs per group anyway: the same transient (the group's dZ
+  // rows) and the same arithmetic per token and per grad_W contraction, with
+  // one projection launch (and one teacher bucketing) per group, so the
+  // partly filled round comes once per group. When a chunk's tiles fill whole
+  // rounds, each chunk's dH right after its own projection measured faster
+  // than one dH over the group.
+  pl.merged = 1;
+  const int64_t proj_tiles = cdiv(pl.c, kTile) * (pl.Vp / kTile);
+  const bool dh_grouped =
+      choose_dh_split(cdiv(pl.c, kTile) * cdiv(pl.D, kTile), pl.Vp * pl.eb / 128) > 1;
+  if (pl.G > 1 && pl.c % kTile == 0 && proj_tiles % 256 != 0 && dh_grouped) {
+    pl.merged = pl.G;
+    pl.c *= pl.G;
+    pl.cp = pl.c;
+    pl.nchunks = cdiv(pl.N, pl.c);
+    pl.nblk = cdiv(pl.c, kLossRows);
+    pl.G = 1;
+  }
   // dH runs per chunk when a chunk's tiles fill the chip, else once per group
   // of G chunks (G times the tiles, dW's grouping); its vocabulary range is
   // split only when the rows it covers still have too few tiles
@@ -148,6 +170,14 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
     }
     pl.off_dhs = part > 0 ? take((size_t)part * pl.D * 4) : 0;
   }
+  // partial tiles of the dW contraction's split last round (when its tiles
+  // leave the last round of the compute units partly filled)
+  {
+    const int64_t tiles = cdiv(pl.D, kTile) * pl.nVT;
+    pl.off_dwp = (tiles > kDwUnits && tiles % kDwUnits != 0)
+                     ? take((size_t)kDwUnits * kTile * kTile * 4)
+                     : 0;
+  }
   pl.total = align256(t);
   return pl;
 }
@@ -157,7 +187,8 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
 // one chunk per group does not fit.
 bool plan_within(const kd_problem* p, size_t cap, Plan* out) {
   Plan pl = make_plan(p);
-  while (pl.total > cap && pl.G > 1) pl = make_plan(p, pl.G - 1);
+  int64_t g = pl.G * pl.merged;  // the caller's chunks per dW group
+  while (pl.total > cap && g > 1) pl = make_plan(p, --g);
   if (pl.total > cap) return false;
   *out = pl;
   return true;
@@ -365,6 +396,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       d.beta = (dw_done || c.accumulate) ? 1 : 0;
       d.gW = c.grad_W;
       d.rowscale = scaled ? fac : nullptr;
+      d.partial = pl.off_dwp ? reinterpret_cast<float*>(ws + pl.off_dwp) : nullptr;
       if (kd_launch_dw(&d, c.stream) != 0) return KD_ERR_DEVICE;
       dw_done = true;
     }

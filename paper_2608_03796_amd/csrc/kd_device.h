@@ -46,11 +46,14 @@ __device__ __forceinline__ int wave_id() {
 // XCD a contiguous range of the linear tile order, so the ~32 tiles an XCD runs
 // at once are neighbours and share operand rows in that XCD's L2; inside the
 // order, tiles are grouped gm at a time along M.
-__device__ __forceinline__ void tile_coords(int pid, int TM, int TN, int gm, int& mt, int& nt) {
-  const int T = TM * TN;
-  const int q = T >> 3, r = T & 7;
+// tile_order_xcd maps pid < n to a position in [0, n) of that order; tile_at
+// maps a position to the tile (mt, nt).
+__device__ __forceinline__ int tile_order_xcd(int pid, int n) {
+  const int q = n >> 3, r = n & 7;
   const int x = pid & 7, k = pid >> 3;
-  const int L = x * q + (x < r ? x : r) + k;
+  return x * q + (x < r ? x : r) + k;
+}
+__device__ __forceinline__ void tile_at(int L, int TM, int TN, int gm, int& mt, int& nt) {
   const int per_group = gm * TN;
   const int g = L / per_group;
   const int first_m = g * gm;
@@ -58,6 +61,9 @@ __device__ __forceinline__ void tile_coords(int pid, int TM, int TN, int gm, int
   const int rem = L - g * per_group;
   mt = first_m + rem % gs;
   nt = rem / gs;
+}
+__device__ __forceinline__ void tile_coords(int pid, int TM, int TN, int gm, int& mt, int& nt) {
+  tile_at(tile_order_xcd(pid, TM * TN), TM, TN, gm, mt, nt);
 }
 
 template <typename T>

@@ -25,19 +25,39 @@
 namespace kd {
 
 // ------------------------------------------------------------------ small --
-__global__ void k_count_valid(const uint8_t* ignore, int64_t N, int* nvalid, float* inv_nvalid) {
-  __shared__ int red[256];
+// N_valid = tokens not ignored, and 1/N_valid (0 if none). One workgroup:
+// 4 mask bytes per load when the mask is 4-byte aligned.
+constexpr int kCountThreads = 1024;
+__global__ __launch_bounds__(kCountThreads) void k_count_valid(const uint8_t* ignore, int64_t N,
+                                                               int* nvalid, float* inv_nvalid) {
+  __shared__ int red[kCountThreads / 64];
+  const int tid = threadIdx.x;
   int c = 0;
-  for (int64_t i = threadIdx.x; i < N; i += 256) c += (ignore == nullptr || ignore[i] == 0) ? 1 : 0;
-  red[threadIdx.x] = c;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if ((int)threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
-    __syncthreads();
+  if (ignore == nullptr) {
+    c = tid == 0 ? (int)N : 0;
+  } else {
+    int64_t i0 = 0;
+    if (((uintptr_t)ignore & 3u) == 0u) {
+      const uint32_t* w = reinterpret_cast<const uint32_t*>(ignore);
+      const int64_t nw = N >> 2;
+      for (int64_t i = tid; i < nw; i += kCountThreads) {
+        const uint32_t v = w[i];
+        c += ((v & 0xffu) == 0u) + (((v >> 8) & 0xffu) == 0u) + (((v >> 16) & 0xffu) == 0u) +
+             ((v >> 24) == 0u);
+      }
+      i0 = nw << 2;
+    }
+    for (int64_t i = i0 + tid; i < N; i += kCountThreads) c += ignore[i] == 0 ? 1 : 0;
   }
-  if (threadIdx.x == 0) {
-    nvalid[0] = red[0];
-    inv_nvalid[0] = red[0] > 0 ? 1.0f / (float)red[0] : 0.0f;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
+  if ((tid & 63) == 0) red[tid >> 6] = c;
+  __syncthreads();
+  if (tid == 0) {
+    int n = 0;
+    for (int w = 0; w < kCountThreads / 64; ++w) n += red[w];
+    nvalid[0] = n;
+    inv_nvalid[0] = n > 0 ? 1.0f / (float)n : 0.0f;
   }
 }
 
@@ -1068,41 +1088,68 @@ __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H,
 // added, and the other half's loads are issued before the first half's stores
 // (loads and stores complete in issue order, so waiting for those loads does
 // not wait for the stores).
-template <typename T>
+//
+// SPLIT (for a tile count that leaves the last round of the 256 compute units
+// partly filled): blocks [0, nfull) compute the whole tiles of the full
+// rounds (in the XCD-aware order over those), and the tail tiles are split
+// into `split` token ranges, block nfull + split q + s taking range s of tail
+// tile nfull + q and storing its fp32 partial tile (pitch 256) at partial
+// slot split q + s; k_dw_fixup then adds the parts to grad_W in a fixed
+// order, so the last round is split times shorter. Without SPLIT every block
+// computes a whole tile (nfull, split and partial unused).
+template <typename T, bool SPLIT>
 __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ Ht, int ldt,
                                                     const T* __restrict__ dZ, int64_t ldz,
                                                     int tokens, int V, int D, int TM, int TN,
-                                                    int beta, float* __restrict__ gW) {
+                                                    int beta, float* __restrict__ gW, int nfull,
+                                                    int split, float* __restrict__ partial) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
+  constexpr int KS = kRowB / (int)sizeof(T);
+  const int nks = ldt / KS;
+  const int pid = blockIdx.x;
+  int L, ks0 = 0, ks1 = nks, slot = -1;
+  if (!SPLIT) {
+    L = tile_order_xcd(pid, TM * TN);
+  } else if (pid < nfull) {
+    L = tile_order_xcd(pid, nfull);
+  } else {
+    const int q = (pid - nfull) / split, s = (pid - nfull) - q * split;
+    L = nfull + q;
+    slot = q * split + s;
+    ks0 = (int)((int64_t)nks * s / split);
+    ks1 = (int)((int64_t)nks * (s + 1) / split);
+  }
   int mt, nt;
-  tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
+  tile_at(L, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;  // m: feature d, n: vocabulary v
   const int eb = Elt<T>::bytes;
   const int lda = ldt * eb, ldb = (int)(ldz * eb);
   const int mrows = min(kTile, D - m0);
-  constexpr int KS = kRowB / (int)sizeof(T);
   AccTile acc;
   gemm_tile<T, KcOp, KmOp, 8, true, 3>(
       KcOp{reinterpret_cast<const char*>(Ht + (int64_t)m0 * ldt), (uint32_t)(mrows * lda), lda},
       KmOp{reinterpret_cast<const char*>(dZ + n0), (int64_t)tokens * ldb - (int64_t)n0 * eb, ldb},
-      0, ldt / KS, lds, acc);
+      ks0, ks1, lds, acc);
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
-  // the tile's rows of grad_W as one resource: rows past V are out of range
-  // (loads give 0, stores are dropped), features past D get an out-of-range
-  // offset
-  const int vrows = __builtin_amdgcn_readfirstlane(min(kTile, V - n0));
+  // the tile's rows of grad_W (or of its partial slot, pitch 256) as one
+  // resource: rows past V are out of range (loads give 0, stores are
+  // dropped), features past D get an out-of-range offset
+  const bool part = SPLIT && slot >= 0;
+  const int pitch = part ? kTile : D;
+  const int vrows = __builtin_amdgcn_readfirstlane(part ? kTile : min(kTile, V - n0));
   const __amdgpu_buffer_rsrc_t ro =
-      make_rsrc(gW + (int64_t)n0 * D, (uint32_t)vrows * (uint32_t)D * 4u);
-  // block (i, j) sits at byte offset obase + 64 i (16 features) + 64 D j (16
-  // rows): the per-lane part is one register, 64 i goes into the
-  // instruction's immediate offset and 64 D j into its scalar offset. D is a
-  // multiple of 64, so whether block i's features exist is the same for the
-  // whole wave.
-  const int dw0 = m0 + wm * 128;
+      part ? make_rsrc(partial + (int64_t)slot * kTile * kTile, (uint32_t)kTile * kTile * 4u)
+           : make_rsrc(gW + (int64_t)n0 * D, (uint32_t)vrows * (uint32_t)D * 4u);
+  // block (i, j) sits at byte offset obase + 64 i (16 features) + 64 pitch j
+  // (16 rows): the per-lane part is one register, 64 i goes into the
+  // instruction's immediate offset and 64 pitch j into its scalar offset. D
+  // is a multiple of 64, so whether block i's features exist is the same for
+  // the whole wave.
+  const int dw0 = (part ? 0 : m0) + wm * 128;
   const uint32_t obase =
-      ((uint32_t)acc_n(wn, 0, lane) * (uint32_t)D + (uint32_t)(dw0 + 4 * (lane >> 4))) * 4u;
-  const uint32_t jstep = 64u * (uint32_t)D;
+      ((uint32_t)acc_n(wn, 0, lane) * (uint32_t)pitch + (uint32_t)(dw0 + 4 * (lane >> 4))) * 4u;
+  const uint32_t jstep = 64u * (uint32_t)pitch;
   auto ld = [&](int i, int j) {
     return __builtin_bit_cast(
         f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ro, obase + 64u * i, jstep * j, 0));
@@ -1111,8 +1158,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ Ht, in
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), ro, obase + 64u * i,
                                            jstep * j, 0);
   };
-  auto live = [&](int i) { return dw0 + 16 * i < D; };
-  if (beta) {
+  auto live = [&](int i) { return part || dw0 + 16 * i < D; };
+  if (beta && !part) {
     f32x4_t old[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -1146,6 +1193,27 @@ __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ Ht, in
 #pragma unroll
         for (int j = 0; j < 4; ++j) st(i, j, acc.v[i][j]);
   }
+}
+
+// The split tail tiles of k_dw: grad_W = (beta ? grad_W : 0) + part 0 + part 1
+// + ... in this order. One thread per 4 features of a vocabulary row of a tail
+// tile (grid: tail tiles x 256 rows x 64 threads).
+__global__ __launch_bounds__(256) void k_dw_fixup(const float* __restrict__ partial, int split,
+                                                  int nfull, int TM, int TN, int V, int D,
+                                                  int beta, float* __restrict__ gW) {
+  const int q = blockIdx.x;                      // tail tile
+  const int row = blockIdx.y * 4 + (threadIdx.x >> 6);
+  const int c4 = (threadIdx.x & 63) * 4;         // first of 4 features in the tile
+  int mt, nt;
+  tile_at(nfull + q, TM, TN, 4, mt, nt);
+  const int v = nt * kTile + row, d = mt * kTile + c4;
+  if (v >= V || d >= D) return;
+  f32x4_t sum = beta ? *reinterpret_cast<const f32x4_t*>(gW + (int64_t)v * D + d)
+                     : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < split; ++s)
+    sum += *reinterpret_cast<const f32x4_t*>(partial + ((int64_t)(q * split + s) * kTile + row) *
+                                                           kTile + c4);
+  *reinterpret_cast<f32x4_t*>(gW + (int64_t)v * D + d) = sum;
 }
 
 // ------------------------------------------------------------ index check --
@@ -1212,12 +1280,12 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 namespace {
 enum ProfKind {
   P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
-  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_ROW_FINISH, P_NKINDS
+  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_ROW_FINISH, P_DW_FIXUP, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
     "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
     "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows", "logits_dz", "ref_logit",
-    "row_finish"};
+    "row_finish", "dw_fixup"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -1428,10 +1496,35 @@ static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
                        a.rowscale);
   }
   const int TM = cdiv(a.D, kTile), TN = cdiv(a.V, kTile);
-  ProfScope ps_(P_DW, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
-  hipLaunchKernelGGL(k_dw<T>, dim3(TM * TN), dim3(kThreads), 0, s, static_cast<const T*>(Ht), ldt,
-                     static_cast<const T*>(a.dZ), a.ldz, (int)a.tokens, (int)a.V, (int)a.D, TM,
-                     TN, a.beta, a.gW);
+  const int tiles = TM * TN;
+  // a partly filled last round of the 256 compute units is split along the
+  // tokens when the host provides the partial tiles' workspace
+  int nfull = tiles, split = 1;
+  const int nks = ldt * (int)sizeof(T) / kRowB;
+  if (a.partial != nullptr && tiles > kDwUnits && tiles % kDwUnits != 0) {
+    const int tail = tiles % kDwUnits;
+    split = std::min(kDwMaxSplit, std::min(kDwUnits / tail, nks));
+    if (split >= 2) nfull = tiles - tail;
+    else split = 1;
+  }
+  {
+    ProfScope ps_(P_DW, 2.0 * (double)a.tokens * (double)a.D * (double)a.V, s);
+    if (nfull < tiles)
+      hipLaunchKernelGGL((k_dw<T, true>), dim3(nfull + (tiles - nfull) * split), dim3(kThreads),
+                         0, s, static_cast<const T*>(Ht), ldt, static_cast<const T*>(a.dZ), a.ldz,
+                         (int)a.tokens, (int)a.V, (int)a.D, TM, TN, a.beta, a.gW, nfull, split,
+                         a.partial);
+    else
+      hipLaunchKernelGGL((k_dw<T, false>), dim3(tiles), dim3(kThreads), 0, s,
+                         static_cast<const T*>(Ht), ldt, static_cast<const T*>(a.dZ), a.ldz,
+                         (int)a.tokens, (int)a.V, (int)a.D, TM, TN, a.beta, a.gW, tiles, 1,
+                         (float*)nullptr);
+  }
+  if (nfull < tiles) {
+    ProfScope ps_(P_DW_FIXUP, 0.0, s);
+    hipLaunchKernelGGL(k_dw_fixup, dim3(tiles - nfull, kTile / 4), dim3(256), 0, s, a.partial,
+                       split, nfull, TM, TN, (int)a.V, (int)a.D, a.beta, a.gW);
+  }
   return (int)hipGetLastError();
 }
 
@@ -1444,7 +1537,7 @@ extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
 {
     ProfScope ps_(P_COUNT_VALID, 0.0, s);
-    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(256), 0, s, a->ignore, a->N, a->nvalid,
+    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(kCountThreads), 0, s, a->ignore, a->N, a->nvalid,
                      a->inv_nvalid);
     }
   if (a->zero_gW != nullptr) {

@@ -84,6 +84,12 @@ struct KdDhArgs {
   const float* rowscale;    // [tokens] factor of each dZ row, or null (= 1)
 };
 
+// dW tiles per full round (the compute units) and the largest split of the
+// tail tiles' token range; the partial tiles' workspace holds
+// kDwUnits * 256 * 256 floats (64 MiB)
+constexpr int kDwUnits = 256;
+constexpr int kDwMaxSplit = 4;
+
 // dW GEMM over the chunks of one group: grad_W (+)= dZ[:tokens]^T H[:tokens]
 struct KdDwArgs {
   int dtype;
@@ -97,6 +103,7 @@ struct KdDwArgs {
   float* gW;
   const float* rowscale;    // [tokens] factor of each dZ row (applied to the
                             // hidden rows), or null (= 1)
+  float* partial;           // workspace of the split tail tiles, or null (no split)
 };
 
 extern "C" {

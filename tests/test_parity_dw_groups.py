@@ -62,3 +62,43 @@ def test_grad_W_full_groups(gpu_lib, N, D, ign):
     assert e_t <= TOL["bf16"]["loss"]
     assert e_h <= TOL["bf16"]["grad"]
     assert e_w <= TOL["bf16"]["grad"]
+
+
+@pytest.mark.parametrize("N,D,V,K,chunk,dtype,ign", [
+    # 300 dW tiles (one full round of 256 and 44 tail tiles split 4 ways),
+    # two groups: the second group's tail tiles add to grad_W (beta = 1)
+    (20000, 64, 76800, 32, 4096, torch.bfloat16, 0.05),
+    # fp32, 274 tiles (18 tail tiles), one group, a ragged vocabulary tile
+    (300, 64, 70000, 8, 100, torch.float32, 0.0),
+])
+def test_grad_W_split_tail(gpu_lib, N, D, V, K, chunk, dtype, ign):
+    """The dW contraction's last, partly filled round of tiles is split along
+    the tokens and its parts are added to grad_W by a fixup pass: every grad_W
+    element against the oracle, and accumulate_grad_W adds a second call's
+    gradient on top (twice the first call's, to fp32 rounding)."""
+    tol = TOL["bf16" if dtype == torch.bfloat16 else "f32"]
+    print(f"[dw-split] N={N} D={D} V={V} K={K} chunk={chunk} {dtype}", flush=True)
+    dev = "cuda"
+    hidden = ki.make_hidden(N, D, dtype, dev, seed=ki.SEED_HIDDEN + 7)
+    W = ki.make_weight(V, D, dtype, dev, seed=ki.SEED_W + 7)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + 7)
+    ignore = None
+    if ign > 0:
+        g = torch.Generator(device="cpu")
+        g.manual_seed(ki.SEED_MASK + 7)
+        ignore = (torch.rand(N, generator=g) < ign).to(torch.uint8).to(dev)
+    out = gpu_lib.fwd_bwd(hidden, W, idx, logit, tau=1.0, ignore=ignore, chunk=chunk)
+    acc = out["grad_W"].clone()
+    gpu_lib.fwd_bwd(hidden, W, idx, logit, tau=1.0, ignore=ignore, chunk=chunk, grad_hidden=False,
+                    grad_W_out=acc, accumulate_grad_W=True)
+    torch.cuda.synchronize()
+    ref = oracle_by_row_blocks(kd_topk_kl, to64(hidden), to64(W), to64(idx), to64(logit), 1.0,
+                               ignore=to64(ignore))
+    e_w = rel_max(to64(out["grad_W"]), ref["grad_W"])
+    e_h = rel_max(to64(out["grad_hidden"]), ref["grad_hidden"])
+    e_a = rel_max(to64(acc), 2.0 * to64(out["grad_W"]))
+    print(f"[dw-split] grad_W {e_w:.2e}, grad_hidden {e_h:.2e}, accumulated {e_a:.2e}",
+          flush=True)
+    assert e_w <= tol["grad"]
+    assert e_h <= tol["grad"]
+    assert e_a <= 1e-6
