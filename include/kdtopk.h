@@ -109,10 +109,15 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  *
  *   hidden        [N, D] dtype        student hidden states h (row t = token t)
  *   W             [V, D] dtype        output projection
- *   teacher_idx   [N, K] int32        support S_t: K distinct indices in [0, V)
- *                                     per row (not range-checked here
- *                                     unless KD_DEBUG_CHECK=1; see
- *                                     kd_topk_kl_check_indices)
+ *   teacher_idx   [N, K] int32        support S_t: K indices in [0, V) per
+ *                                     row (not range-checked here unless
+ *                                     KD_DEBUG_CHECK=1; see
+ *                                     kd_topk_kl_check_indices). An index
+ *                                     outside [0, V) is skipped; an index
+ *                                     repeated in a row counts once with the
+ *                                     sum of the repeated entries'
+ *                                     probabilities (the dense teacher row
+ *                                     of §3.2.1)
  *   teacher_logit [N, K] fp32         teacher logits of the support; the
  *                                     teacher distribution is their softmax
  *                                     over the K entries at temperature tau
@@ -232,7 +237,9 @@ kd_status kd_topk_kl_bwd(const kd_problem* p,
 
 /*
  * Checks that every teacher index lies in [0, V) and that no row repeats an
- * index (the support S_t of §3.2 is a set). Synchronises `hip_stream`.
+ * index (the support S_t of §3.2 is a set; the loss accepts repeats and sums
+ * them, but a top-K cache never repeats an index, so a repeat points at a
+ * broken cache). Synchronises `hip_stream`.
  * Returns KD_OK, KD_ERR_BAD_INDEX, or an argument/device error. Uses the
  * first bytes of `workspace` (same size rule as kd_topk_kl_fwd_bwd).
  *

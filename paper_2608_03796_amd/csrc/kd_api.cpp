@@ -44,7 +44,7 @@ struct Plan {
   bool prep_per_group; // rows prepared once per group (chunks of whole 256-token tiles)
   int64_t ng;          // rows of the per-row arrays: the group's, or one chunk's (padded)
   int64_t td, ksteps;  // dH column tiles and K steps (for its vocabulary split)
-  size_t off_misc, off_p, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
+  size_t off_misc, off_p, off_tidx, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
       off_lossp, off_dz, off_fac, off_ht, off_dhs, off_dwp, total;
 };
 
@@ -148,6 +148,7 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
   };
   pl.off_misc = take(256);
   pl.off_p = take((size_t)pl.ng * pl.K * 4);
+  pl.off_tidx = take((size_t)pl.ng * pl.K * 4);
   pl.off_rows = take((size_t)7 * pl.ng * 4);
   pl.off_pm = take((size_t)pl.cp * pl.nVT * 4);
   pl.off_ps = take((size_t)pl.cp * pl.nVT * 4);
@@ -320,7 +321,8 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.inv_tau = 1.0f / p->temperature;
     a.W = c.W;
     a.Hc = static_cast<const char*>(c.hidden) + row0 * pl.D * pl.eb;
-    a.tidx = c.idx + row0 * pl.K;
+    a.tidx_in = c.idx + row0 * pl.K;
+    a.tidx = reinterpret_cast<int32_t*>(ws + pl.off_tidx) + o * pl.K;
     a.tlogit = c.tlogit;
     a.ignore = c.ignore;
     a.inv_nvalid = inv_nvalid;

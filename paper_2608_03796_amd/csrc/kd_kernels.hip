@@ -74,17 +74,41 @@ __global__ void k_fill_f32(float* p, int64_t n, float v) {
 // mean (gscale, default 1), or the upstream gradient of the token's own loss
 // (gtok); 0 for ignored rows. With a saved log-normaliser (backward only) the
 // row's log2 Z is set from it. One wave per row.
-__global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, int64_t row0,
-                                   int rows, int K, float inv_tau, int logprobs,
-                                   const float* inv_nvalid, const float* gscale,
-                                   const float* gtok, const float* logz_in, float* p_out,
-                                   float* rowM, float* rowH, float* rowCoef, float* rowCoefM,
-                                   float* rowL2) {
+//
+// The support is a set; a row that repeats an index is read as the dense
+// teacher row that sums the repeated entries (scatter-add): the first
+// occurrence carries the sum of their probabilities (in entry order), H takes
+// P log P of that sum, and the later occurrences get p = 0 and the index -1 in
+// tidx_out, the row's copy of its indices that every later kernel reads (an
+// index outside [0, V) is skipped everywhere). Rows without repeats are
+// unchanged. Repeats are found with a hash set of the row's indices in LDS
+// (an insertion that meets its own index); only a wave in which some row
+// repeats an index compares the row's entries pairwise, in entry order.
+// LDS hash set of the row's valid indices (power-of-two slots, at least K):
+// size in ints for K entries
+__host__ __device__ constexpr int prologue_hash_slots(int K) {
+  int t = 64;
+  while (t < 2 * K && t < 4096) t *= 2;
+  return t;
+}
+
+__global__ __launch_bounds__(64) void k_teacher_prologue(
+    const int32_t* __restrict__ tidx, int32_t* __restrict__ tidx_out, const float* tlogit,
+    const uint8_t* ignore, int64_t row0, int rows, int K, int V, float inv_tau, int logprobs,
+    const float* inv_nvalid, const float* gscale, const float* gtok, const float* logz_in,
+    float* p_out, float* rowM, float* rowH, float* rowCoef, float* rowCoefM, float* rowL2) {
+  extern __shared__ __attribute__((aligned(16))) char psm[];
+  const int T = prologue_hash_slots(K);
+  int* hset = reinterpret_cast<int*>(psm);
+  int* sidx = hset + T;
+  float* sp = reinterpret_cast<float*>(sidx + K);
   const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + wave_id();
+  const int r = blockIdx.x;
   if (r >= rows) return;
   const int64_t t = row0 + r;
   const float* u = tlogit + t * (int64_t)K;
+  const int32_t* ix = tidx + (int64_t)r * K;
+  for (int i = lane; i < T; i += 64) hset[i] = -1;
   float mx = 0.f, logs = 0.f, scale = 1.f;
   if (!logprobs) {
     mx = -INFINITY;
@@ -96,13 +120,62 @@ __global__ void k_teacher_prologue(const float* tlogit, const uint8_t* ignore, i
     logs = logf(s);
     scale = inv_tau;
   }
-  float m = 0.f, h = 0.f;
+  __syncthreads();  // the cleared hash set
+  // p, and the row's indices into the hash set: an insertion that finds its
+  // own index already there has seen a repeat (invalid indices are skipped
+  // by every kernel and take no part)
+  float m = 0.f;
+  bool seen = false;
   for (int k = lane; k < K; k += 64) {
-    const float lp = u[k] * scale - mx - logs;
-    const float pk = expf(lp);
-    p_out[(int64_t)r * K + k] = pk;
+    const float pk = expf(u[k] * scale - mx - logs);
+    const int v = ix[k];
+    sidx[k] = v;
+    sp[k] = pk;
     m += pk;
-    h += pk > 0.f ? pk * lp : 0.f;
+    if ((unsigned)v < (unsigned)V) {
+      uint32_t h = ((uint32_t)v * 2654435761u) >> 7;
+      for (int probe = 0; probe < T; ++probe, ++h) {
+        const int prev = atomicCAS(&hset[h & (T - 1)], -1, v);
+        if (prev == -1) break;
+        if (prev == v) {
+          seen = true;
+          break;
+        }
+      }
+    }
+  }
+  const bool any_repeat = __builtin_amdgcn_ballot_w64(seen) != 0ull;
+  __syncthreads();  // sidx and sp of the whole row
+  float h = 0.f;
+  for (int k = lane; k < K; k += 64) {
+    const int v = sidx[k];
+    const float pk = sp[k];
+    bool dup = false;
+    float acc = pk;
+    if (any_repeat) {
+      // rare: an entry repeats an earlier index (p = 0, index -1) or is the
+      // first of repeats (their probabilities summed in entry order)
+      if ((unsigned)v < (unsigned)V) {
+        for (int j = 0; j < K; ++j) {
+          if (j != k && sidx[j] == v) {
+            if (j < k) dup = true;
+            else acc += sp[j];
+          }
+        }
+      }
+    }
+    const float lp = u[k] * scale - mx - logs;
+    float pe = pk, term = pk > 0.f ? pk * lp : 0.f;
+    if (dup) {
+      pe = 0.f;
+      term = 0.f;
+    } else if (acc != pk) {
+      pe = acc;
+      term = acc > 0.f ? acc * logf(acc) : 0.f;
+    }
+    p_out[(int64_t)r * K + k] = pe;
+    tidx_out[(int64_t)r * K + k] = dup ? -1 : v;
+    h += term;
   }
   m = wave_sum(m);
   h = wave_sum(h);
@@ -1384,10 +1457,12 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
   if (a.stages & KD_STAGE_PREP) {
     {
       ProfScope ps_(P_PROLOGUE, 0.0, s);
-      hipLaunchKernelGGL(k_teacher_prologue, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.tlogit,
-                         a.ignore, a.row0, a.rows, a.K, a.inv_tau, a.teacher_logprobs,
-                         a.inv_nvalid, a.gscale, a.gtok, fwd ? nullptr : a.logz_in, a.p, a.rowM,
-                         a.rowH, a.rowCoef, a.rowCoefM, a.rowL2);
+      hipLaunchKernelGGL(k_teacher_prologue, dim3(a.rows), dim3(64),
+                         (size_t)4 * prologue_hash_slots(a.K) + (size_t)8 * a.K, s, a.tidx_in,
+                         a.tidx, a.tlogit, a.ignore, a.row0, a.rows, a.K, (int)a.V, a.inv_tau,
+                         a.teacher_logprobs, a.inv_nvalid, a.gscale, a.gtok,
+                         fwd ? nullptr : a.logz_in, a.p, a.rowM, a.rowH, a.rowCoef, a.rowCoefM,
+                         a.rowL2);
     }
     {
       ProfScope ps_(P_BUCKET, 0.0, s);

@@ -45,7 +45,8 @@ struct KdChunkArgs {
   float inv_tau;
   const void* W;            // [V, D]
   const void* Hc;           // hidden + row0 * D
-  const int32_t* tidx;      // teacher_idx + row0 * K
+  const int32_t* tidx_in;   // teacher_idx + row0 * K (the caller's)
+  int32_t* tidx;            // [rows, K] the prologue's copy (repeats -1), read by the rest
   const float* tlogit;      // full [N, K] (prologue indexes with row0)
   const uint8_t* ignore;    // full [N] or null
   const float* inv_nvalid;

@@ -111,3 +111,29 @@ def test_partial_mass_autograd(tau):
     assert out["loss"] == pytest.approx(float(loss), rel=1e-12)
     np.testing.assert_allclose(out["grad_hidden"], th.grad.numpy(), rtol=1e-10, atol=1e-13)
     np.testing.assert_allclose(out["grad_W"], tW.grad.numpy(), rtol=1e-10, atol=1e-13)
+
+
+@pytest.mark.parametrize("tau", [1.0, 0.7])
+def test_repeated_index_equals_merged_entry(tau):
+    """A row that lists a vocabulary entry twice, with teacher logits t1 and t2,
+    is the row that lists it once with the logit tau * logaddexp(t1/tau, t2/tau)
+    (its softmax weight is the sum of the two): loss, per-token loss and both
+    gradients agree. Pins the oracle's reading of repeats (the dense teacher row
+    sums them) against a construction that has no repeat."""
+    rng = np.random.default_rng(5)
+    N, D, V, K = 6, 8, 40, 5
+    h = rng.standard_normal((N, D))
+    W = rng.standard_normal((V, D)) * 0.3
+    idx = np.stack([rng.choice(V, K, replace=False) for _ in range(N)])
+    tl = rng.standard_normal((N, K)) * 2
+    rep = idx.copy()
+    rep[:, 3] = rep[:, 1]                           # entry 3 repeats entry 1's index
+    merged_idx = np.delete(idx, 3, axis=1)
+    merged_tl = np.delete(tl, 3, axis=1)
+    merged_tl[:, 1] = tau * np.logaddexp(tl[:, 1] / tau, tl[:, 3] / tau)
+    a = kd_topk_kl(h, W, rep, tl, tau=tau)
+    b = kd_topk_kl(h, W, merged_idx, merged_tl, tau=tau)
+    assert abs(a["loss"] - b["loss"]) < 1e-12
+    np.testing.assert_allclose(a["loss_per_token"], b["loss_per_token"], atol=1e-12)
+    np.testing.assert_allclose(a["grad_hidden"], b["grad_hidden"], atol=1e-12)
+    np.testing.assert_allclose(a["grad_W"], b["grad_W"], atol=1e-12)

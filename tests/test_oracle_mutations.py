@@ -32,6 +32,8 @@ MUTATIONS = {
     "grad_h_transposed_head": ("grad_h[s0:s1] = G @ W", "grad_h[s0:s1] = (G @ W) * 0.5"),
     "scatter_overwrite_first_col": ("np.add.at(P,", "np.add.at(P[:, ::-1],"),
     "ignored_rows_counted": ("ell[~valid[s0:s1]] = 0.0", "pass"),
+    "scatter_assigns_repeats": ("np.add.at(P, (np.repeat(rows, K), idx[s0:s1].reshape(-1)),",
+                                "P.__setitem__((np.repeat(rows, K), idx[s0:s1].reshape(-1)),"),
     "token_weights_ignored": ("g = np.where(valid, _f64(token_weights), 0.0)",
                               "g = np.where(valid, 1.0 / max(n_valid, 1.0), 0.0)"),
     "logprobs_renormalised": ("return np.exp(_f64(teacher_logit))",
@@ -118,6 +120,19 @@ def _pins(fn):
         ok = False
     if not ok:
         failed.append("partial-mass autograd")
+    # a repeated index is the merged entry tau * logaddexp(t1/tau, t2/tau)
+    try:
+        rep = idx.copy()
+        rep[:, 3] = rep[:, 1]
+        mi, mt = np.delete(idx, 3, axis=1), np.delete(tl, 3, axis=1)
+        mt[:, 1] = tau * np.logaddexp(tl[:, 1] / tau, tl[:, 3] / tau)
+        a, b = fn(h, W, rep, tl, tau=tau), fn(h, W, mi, mt, tau=tau)
+        ok = (abs(a["loss"] - b["loss"]) < 1e-12
+              and np.allclose(a["grad_W"], b["grad_W"], atol=1e-12))
+    except Exception:
+        ok = False
+    if not ok:
+        failed.append("repeat = merged entry")
     return failed
 
 

@@ -102,3 +102,38 @@ def test_grad_W_split_tail(gpu_lib, N, D, V, K, chunk, dtype, ign):
     assert e_w <= tol["grad"]
     assert e_h <= tol["grad"]
     assert e_a <= 1e-6
+
+
+def test_merged_chunks_with_short_last_group(gpu_lib):
+    """Chunks whose projection leaves the last round of tiles partly filled
+    (2 x 196 = 392 tiles per 512-token chunk) while dH runs per group are
+    processed as one chunk per dW group: 20000 tokens in chunks of 512 run as
+    16384 + 3616 tokens. Every output against the oracle; the loss and the
+    per-token losses equal those of a chunk size that is not merged (100)."""
+    N, D, V, K, chunk, tau = 20000, 64, 50000, 16, 512, 2.0
+    dev = "cuda"
+    hidden = ki.make_hidden(N, D, torch.bfloat16, dev, seed=ki.SEED_HIDDEN + 9)
+    W = ki.make_weight(V, D, torch.bfloat16, dev, seed=ki.SEED_W + 9)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + 9)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(ki.SEED_MASK + 9)
+    ignore = (torch.rand(N, generator=g) < 0.05).to(torch.uint8).to(dev)
+    out = gpu_lib.fwd_bwd(hidden, W, idx, logit, tau=tau, ignore=ignore, chunk=chunk,
+                          loss_per_token=True)
+    other = gpu_lib.fwd_bwd(hidden, W, idx, logit, tau=tau, ignore=ignore, chunk=100,
+                            loss_per_token=True, grad_hidden=False, grad_W=False)
+    torch.cuda.synchronize()
+    ref = oracle_by_row_blocks(kd_topk_kl, to64(hidden), to64(W), to64(idx), to64(logit), tau,
+                               ignore=to64(ignore))
+    e_l = abs(float(out["loss"]) - ref["loss"]) / abs(ref["loss"])
+    e_t = rel_max(to64(out["loss_per_token"]), ref["loss_per_token"])
+    e_h = rel_max(to64(out["grad_hidden"]), ref["grad_hidden"])
+    e_w = rel_max(to64(out["grad_W"]), ref["grad_W"])
+    print(f"[merged] loss rel {e_l:.2e}, l_t {e_t:.2e}, grad_hidden {e_h:.2e}, grad_W {e_w:.2e}",
+          flush=True)
+    assert e_l <= TOL["bf16"]["loss"] and e_t <= TOL["bf16"]["loss"]
+    assert e_h <= TOL["bf16"]["grad"] and e_w <= TOL["bf16"]["grad"]
+    # the per-token arithmetic does not depend on the chunking
+    lt, lo = out["loss_per_token"], other["loss_per_token"]
+    assert rel_max(to64(lt), to64(lo)) <= 1e-6
+    assert torch.equal(lt[ignore.bool()], torch.zeros_like(lt[ignore.bool()]))

@@ -270,3 +270,48 @@ def test_check_indices(gpu_lib):
     dup = idx.clone()
     dup[123, 7] = dup[123, 2]
     assert not gpu_lib.check_indices(dup, V=1000)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("logprobs", [False, True])
+def test_repeated_teacher_indices(gpu_lib, dtype, logprobs):
+    """Rows that repeat a teacher index (twice, three times; the repeats far
+    apart or adjacent) read as the dense teacher row that sums the repeated
+    entries, as the oracle's scatter-add builds it: the fused call and the
+    split entry points against the oracle, every output."""
+    kd = gpu_lib
+    N, D, V, K, chunk, tau = 300, 64, 2000, 12, 128, 1.5
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    inp = _inputs(N, D, V, K, tdt, seed=33, ignore_frac=0.1)
+    idx = inp["teacher_idx"].cpu().clone()
+    g = torch.Generator(device="cpu")
+    g.manual_seed(ki.SEED_TEACHER + 33)
+    rows = torch.randperm(N, generator=g)[:100]
+    for n, r in enumerate(rows.tolist()):
+        a, b = sorted(torch.randperm(K, generator=g)[:2].tolist())
+        idx[r, b] = idx[r, a]                 # a pair
+        if n % 3 == 0:
+            c = int(torch.randint(0, K, (1,), generator=g))
+            idx[r, c] = idx[r, a]             # possibly a triple
+    inp["teacher_idx"] = idx.to("cuda").contiguous()
+    assert not kd.check_indices(inp["teacher_idx"], V)
+    if logprobs:
+        u = inp["teacher_logit"]
+        inp["teacher_logit"] = (torch.log_softmax(u, dim=1) - 0.3).contiguous()
+    tol = TOL[dtype]
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk,
+                     teacher_mode="logprobs" if logprobs else "logits")
+    args = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+    fb = kd.fwd_bwd(*args, tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True,
+                    teacher_logprobs=logprobs)
+    f = kd.fwd(*args, tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True,
+               teacher_logprobs=logprobs)
+    b = kd.bwd(*args, f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk,
+               teacher_logprobs=logprobs)
+    torch.cuda.synchronize()
+    for res in (fb, f):
+        assert abs(float(res["loss"]) - ref["loss"]) <= tol["loss"] * abs(ref["loss"])
+        assert rel_max(to64(res["loss_per_token"]), ref["loss_per_token"]) <= tol["loss"]
+    for res in (fb, b):
+        assert rel_max(to64(res["grad_hidden"]), ref["grad_hidden"]) <= tol["grad"]
+        assert rel_max(to64(res["grad_W"]), ref["grad_W"]) <= tol["grad"]
