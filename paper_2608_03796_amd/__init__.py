@@ -316,11 +316,12 @@ def fwd(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore=None,
 def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ignore=None,
         chunk: int = 4096, grad_loss=None, grad_loss_per_token=None, grad_hidden: bool = True,
         grad_W: bool = True, grad_W_out=None, accumulate_grad_W: bool = False, workspace=None,
-        teacher_logprobs: bool = False):
+        teacher_logprobs: bool = False, grad_hidden_f32: bool = False):
     """kd_topk_kl_bwd: gradients from the saved log-normaliser. grad_loss is the
     upstream gradient of the mean loss (0-d fp32 device tensor, None = 1);
     grad_loss_per_token [N] fp32 replaces it with per-token upstream gradients.
-    Returns a dict with 'grad_hidden' and 'grad_W' as requested."""
+    Returns a dict with 'grad_hidden' (hidden's dtype, or fp32 with
+    grad_hidden_f32) and 'grad_W' as requested."""
     import torch
     lib = load_library()
     N, D, V, K, dt = _check_inputs(hidden, W, teacher_idx, teacher_logit, ignore)
@@ -334,12 +335,13 @@ def bwd(hidden, W, teacher_idx, teacher_logit, saved_logz, tau: float = 1.0, ign
         _check_tensor("grad_loss_per_token", grad_loss_per_token, (N,), torch.float32, dev)
     res = {}
     if grad_hidden:
-        res["grad_hidden"] = torch.empty(N, D, dtype=hidden.dtype, device=dev)
+        res["grad_hidden"] = torch.empty(N, D, device=dev,
+                                         dtype=torch.float32 if grad_hidden_f32 else hidden.dtype)
     if grad_W:
         res["grad_W"] = grad_W_out if grad_W_out is not None else torch.empty(
             V, D, dtype=torch.float32, device=dev)
         _check_tensor("grad_W", res["grad_W"], (V, D), torch.float32, dev)
-    pr = problem(N, D, V, K, chunk, tau, dt, _flags(teacher_logprobs))
+    pr = problem(N, D, V, K, chunk, tau, dt, _flags(teacher_logprobs, grad_hidden_f32))
     if workspace is None:
         workspace = alloc_workspace(N, D, V, K, chunk, tau, dt, dev)
     _check_workspace(workspace, dev)

@@ -298,3 +298,29 @@ def test_scale_grads(gpu_lib, n):
     torch.cuda.synchronize()
     assert torch.equal(out32.cpu(), ref)
     assert torch.equal(out_bf2.cpu(), ref2.to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("chunk", [100, 300])
+def test_grad_hidden_f32_flag(gpu_lib, chunk):
+    """KD_FLAG_GRAD_HIDDEN_F32 (fused call and split backward): grad_hidden in
+    fp32, whose single rounding to bf16 is bitwise the bf16 grad_hidden of the
+    same call without the flag; the fp32 values match the oracle. chunk 100
+    runs dH with a split vocabulary range (fp32 partials reduced), 300 without."""
+    kd = gpu_lib
+    N, D, V, K, tau = 600, 128, 4133, 7, 1.3
+    inp = _inputs(N, D, V, K, torch.bfloat16, seed=44, ignore_frac=0.1)
+    a = (inp["hidden"], inp["W"], inp["teacher_idx"], inp["teacher_logit"])
+    fb16 = kd.fwd_bwd(*a, tau=tau, ignore=inp["ignore"], chunk=chunk, grad_W=False)
+    fb32 = kd.fwd_bwd(*a, tau=tau, ignore=inp["ignore"], chunk=chunk, grad_W=False,
+                      grad_hidden_f32=True)
+    f = kd.fwd(*a, tau=tau, ignore=inp["ignore"], chunk=chunk)
+    b16 = kd.bwd(*a, f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk, grad_W=False)
+    b32 = kd.bwd(*a, f["saved_logz"], tau=tau, ignore=inp["ignore"], chunk=chunk, grad_W=False,
+                 grad_hidden_f32=True)
+    torch.cuda.synchronize()
+    assert fb32["grad_hidden"].dtype == torch.float32 and b32["grad_hidden"].dtype == torch.float32
+    assert torch.equal(fb32["grad_hidden"].to(torch.bfloat16), fb16["grad_hidden"])
+    assert torch.equal(b32["grad_hidden"].to(torch.bfloat16), b16["grad_hidden"])
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk)
+    for res in (fb32, b32):
+        assert rel_max(to64(res["grad_hidden"]), ref["grad_hidden"]) <= TOL["bf16"]["grad"]

@@ -12,6 +12,7 @@ library's static scratch, each smaller than the one before:
   3. fp32, N=300, D=128, V=4133, K=7, chunk 100, tau 2, 20% ignored: bitwise.
 
 The stale contents each call leaves in the scratch must not leak into the next.
+Then the use it exists for: the call captured into a HIP graph and replayed.
 """
 import pytest
 import torch
@@ -71,3 +72,42 @@ def test_noalloc_matches_fwd_bwd(gpu_lib):
             print(f"[noalloc] call {n + 1}: capped plan, grad_hidden {e_h:.2e}, "
                   f"grad_W {e_w:.2e}", flush=True)
             assert e_h <= tol and e_w <= tol
+
+
+def test_noalloc_call_in_a_graph(gpu_lib):
+    """The allocation-free call captured into a HIP graph (torch.cuda.graph) and
+    replayed three times, with other eager work (a call through the workspace
+    entry point on other inputs, and fills of the outputs) between the replays:
+    every replay rewrites every output bitwise equal to the eager call's."""
+    kd = gpu_lib
+    N, D, V, K, chunk, tau = 1000, 256, 50000, 32, 256, 1.5
+    dev = "cuda"
+    h = ki.make_hidden(N, D, torch.bfloat16, dev, seed=ki.SEED_HIDDEN + 61)
+    W = ki.make_weight(V, D, torch.bfloat16, dev, seed=ki.SEED_W + 61)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + 61)
+    h2 = ki.make_hidden(N, D, torch.bfloat16, dev, seed=ki.SEED_HIDDEN + 62)
+
+    def outs():
+        return {"loss": torch.empty((), dtype=torch.float32, device=dev),
+                "loss_per_token": torch.empty(N, dtype=torch.float32, device=dev),
+                "grad_hidden": torch.empty(N, D, dtype=torch.bfloat16, device=dev),
+                "grad_W": torch.empty(V, D, dtype=torch.float32, device=dev)}
+    eager = kd.fwd_bwd_noalloc(h, W, idx, logit, tau=tau, chunk=chunk, out=outs(),
+                               loss_per_token=True)
+    torch.cuda.synchronize()
+    out = outs()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        kd.fwd_bwd_noalloc(h, W, idx, logit, tau=tau, chunk=chunk, out=out, loss_per_token=True)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in out.values():
+            t.fill_(float("nan"))
+        other = kd.fwd_bwd(h2, W, idx, logit, tau=tau, chunk=chunk)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        print(f"[graph] replay {rep}: loss {float(out['loss']):.6f}", flush=True)
+        for k in out:
+            assert torch.equal(out[k], eager[k]), (rep, k)
+        assert not torch.equal(other["grad_W"], eager["grad_W"])
