@@ -401,7 +401,7 @@ def main():
         blas_reference(args.workload)
         return
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} is not supported: this build runs the loss on one "
+        print(f"bench.py: --gpus {args.gpus} is not supported: the library runs the loss on one "
               f"GPU only (no collectives); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     import torch
