@@ -111,3 +111,34 @@ def test_noalloc_call_in_a_graph(gpu_lib):
         for k in out:
             assert torch.equal(out[k], eager[k]), (rep, k)
         assert not torch.equal(other["grad_W"], eager["grad_W"])
+
+
+def test_noalloc_debug_index_check(gpu_lib, monkeypatch):
+    """KD_DEBUG_CHECK=1 on the allocation-free call: the index check runs in the
+    static scratch first; an index outside [0, V) gives KD_ERR_BAD_INDEX with no
+    output touched, valid indices the same outputs as without the check."""
+    kd = gpu_lib
+    N, D, V, K, chunk = 300, 64, 1000, 20, 128
+    dev = "cuda"
+    h = ki.make_hidden(N, D, torch.float32, dev, seed=ki.SEED_HIDDEN + 71)
+    W = ki.make_weight(V, D, torch.float32, dev, seed=ki.SEED_W + 71)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + 71)
+    ref = kd.fwd_bwd_noalloc(h, W, idx, logit, chunk=chunk)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("KD_DEBUG_CHECK", "1")
+    out = kd.fwd_bwd_noalloc(h, W, idx, logit, chunk=chunk)
+    torch.cuda.synchronize()
+    for k in ref:
+        assert torch.equal(out[k], ref[k]), k
+    bad = idx.clone()
+    bad[123, 4] = V
+    sentinel = {"loss": torch.full((), 7.0, device=dev),
+                "grad_hidden": torch.full((N, D), 7.0, device=dev),
+                "grad_W": torch.full((V, D), 7.0, device=dev)}
+    with pytest.raises(kd.KdError) as e:
+        kd.fwd_bwd_noalloc(h, W, bad, logit, chunk=chunk, out=sentinel)
+    assert e.value.code == 6
+    torch.cuda.synchronize()
+    for t in sentinel.values():
+        assert bool((t == 7.0).all())
+    monkeypatch.delenv("KD_DEBUG_CHECK")
