@@ -948,17 +948,42 @@ __global__ __launch_bounds__(256) void k_row_finish(
   if (r < rows) {
     const float* pm = part_m + (int64_t)r * nVT;
     const float* ps = part_s + (int64_t)r * nVT;
+    // up to 512 vocabulary tiles: the row's partials are loaded into registers
+    // in one batch, with the row scalars, before any arithmetic (one round of
+    // memory latency instead of one per pass); the sums keep the same order
+    constexpr int kRF = 8;
+    const bool in_regs = nVT <= 64 * kRF;
+    float pmv[kRF], psv[kRF];
+    if (in_regs) {
+#pragma unroll
+      for (int i = 0; i < kRF; ++i) {
+        const int j = lane + 64 * i;
+        pmv[i] = j < nVT ? pm[j] : -INFINITY;
+        psv[i] = j < nVT ? ps[j] : 0.f;
+      }
+    }
+    const float cm = rowCoefM[r], cf = rowCoef[r];
     float mx = -INFINITY;
-    for (int j = lane; j < nVT; j += 64) mx = fmaxf(mx, pm[j]);
+    if (in_regs) {
+#pragma unroll
+      for (int i = 0; i < kRF; ++i) mx = fmaxf(mx, pmv[i]);
+    } else {
+      for (int j = lane; j < nVT; j += 64) mx = fmaxf(mx, pm[j]);
+    }
     mx = wave_max(mx);
     float s = 0.f;
-    for (int j = lane; j < nVT; j += 64) {
-      const float m = pm[j];
-      if (m != -INFINITY) s += ps[j] * fast_exp2(m - mx);
+    if (in_regs) {
+#pragma unroll
+      for (int i = 0; i < kRF; ++i)
+        if (pmv[i] != -INFINITY) s += psv[i] * fast_exp2(pmv[i] - mx);
+    } else {
+      for (int j = lane; j < nVT; j += 64) {
+        const float m = pm[j];
+        if (m != -INFINITY) s += ps[j] * fast_exp2(m - mx);
+      }
     }
     s = wave_sum(s);
     const float L2 = mx + log2f(s);
-    const float cm = rowCoefM[r], cf = rowCoef[r];
     const float f = cm * fast_exp2(mx - L2);
     if (lane == 0) {
       rowL2[r] = L2;
@@ -1013,14 +1038,18 @@ __global__ __launch_bounds__(256) void k_row_finish(
   if (threadIdx.x == 0) block_partial[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-__global__ void k_finalize_loss(const float* partials, int n, const float* inv_nvalid,
-                                float* loss) {
-  __shared__ float red[256];
+// loss = (sum of the loss partials) / N_valid, in a fixed order: thread i sums
+// partials i, i + 1024, ..., then a tree over the threads.
+constexpr int kFinThreads = 1024;
+__global__ __launch_bounds__(kFinThreads) void k_finalize_loss(const float* partials, int n,
+                                                               const float* inv_nvalid,
+                                                               float* loss) {
+  __shared__ float red[kFinThreads];
   float s = 0.f;
-  for (int i = threadIdx.x; i < n; i += 256) s += partials[i];
+  for (int i = threadIdx.x; i < n; i += kFinThreads) s += partials[i];
   red[threadIdx.x] = s;
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
+  for (int o = kFinThreads / 2; o > 0; o >>= 1) {
     if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
     __syncthreads();
   }
@@ -1631,7 +1660,8 @@ extern "C" int kd_launch_finalize(const float* partials, int n, const float* inv
   hipStream_t s = static_cast<hipStream_t>(stream);
 {
     ProfScope ps_(P_FINALIZE, 0.0, s);
-    hipLaunchKernelGGL(k_finalize_loss, dim3(1), dim3(256), 0, s, partials, n, inv_nvalid, loss);
+    hipLaunchKernelGGL(k_finalize_loss, dim3(1), dim3(kFinThreads), 0, s, partials, n, inv_nvalid,
+                       loss);
     }
   return (int)hipGetLastError();
 }
