@@ -95,10 +95,11 @@ typedef struct kd_problem {
 /*
  * Bytes of device workspace kd_topk_kl_fwd_bwd, kd_topk_kl_fwd,
  * kd_topk_kl_bwd and kd_topk_kl_check_indices need for problem *p. Pure host
- * function: touches no device. The size is O(N/4 + G C_s V + C_s (D + K)),
+ * function: touches no device. The size is O(N/4 + G C_s (V + K) + D G C_s),
  * with G C_s <= 16384 the tokens whose dZ rows one grad_W contraction
- * gathers: it grows with N only through an array of loss partials (one per
- * 4 tokens), never as N*V.
+ * gathers (at most 4 GiB of them), plus 64 MiB when grad_W's tiles leave the
+ * last round of the compute units partly filled: it grows with N only
+ * through an array of loss partials (one per 4 tokens), never as N*V.
  * Errors: KD_ERR_NULL_PTR if p or bytes is NULL; the shape/argument errors of
  * kd_topk_kl_fwd_bwd otherwise.
  */
