@@ -45,7 +45,7 @@ struct Plan {
   int64_t ng;          // rows of the per-row arrays: the group's, or one chunk's (padded)
   int64_t td, ksteps;  // dH column tiles and K steps (for its vocabulary split)
   size_t off_misc, off_p, off_tidx, off_rows, off_pm, off_ps, off_hits, off_hitp, off_hoff, off_zhit,
-      off_lossp, off_dz, off_fac, off_ht, off_dhs, off_dwp, total;
+      off_lossp, off_dz, off_fac, off_ht, off_rowmap, off_dhs, off_dwp, total;
 };
 
 kd_status check_problem(const kd_problem* p) {
@@ -160,8 +160,11 @@ Plan make_plan(const kd_problem* p, int64_t g_max = 0) {
   pl.off_dz = take((size_t)pl.G * pl.c * pl.Vp * pl.eb);
   // factor of each dZ row of the group in the single-projection schedule
   pl.off_fac = take((size_t)pl.G * pl.c * 4);
-  // the hidden rows of one dW group, transposed (tokens padded to 64)
+  // the hidden rows of one dW group, transposed (tokens padded to 64); until
+  // the group's dW it holds the group's tokens that are not ignored, as rows
   pl.off_ht = take((size_t)pl.D * rup(pl.G * pl.c, 64) * pl.eb);
+  // the token of each of those rows
+  pl.off_rowmap = take((size_t)pl.G * pl.c * 4);
   {
     int64_t part = 0;
     for (int64_t r : dh_rows) {
@@ -298,11 +301,20 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
   // the single-projection schedule stores dZ up to a factor per row, which
   // dH applies to its rows and dW to the hidden rows
   const bool scaled = fwd && bwd && (want_dh || want_dw);
+  // With a mask, that schedule leaves the ignored tokens out (their loss and
+  // gradient rows are 0): each dW group's other tokens are gathered first,
+  // and the group's rows are those tokens in order, then rows without a
+  // token, whose tiles the contractions skip (their count is on the device).
+  const bool compact = scaled && c.ignore != nullptr;
+  int* rowmap = reinterpret_cast<int*>(ws + pl.off_rowmap);
+  int* gnrow = reinterpret_cast<int*>(ws + pl.off_misc + 16);
+  char* hcomp = ws + pl.off_ht;
   int64_t n_partials = 0;
   int64_t group_tokens = 0;
   bool dw_done = false;
-  // the per-row arrays from row `o` of the prepared rows
-  auto chunk_args = [&](int64_t row0, int rcount, int64_t o, int stages) {
+  // the per-row arrays from row `o` of the prepared rows; `g` = the row of
+  // the chunk within its dW group
+  auto chunk_args = [&](int64_t row0, int rcount, int64_t o, int64_t g, int stages) {
     KdChunkArgs a{};
     a.dtype = p->dtype;
     a.mode = c.mode;
@@ -320,12 +332,17 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.rows = rcount;
     a.inv_tau = 1.0f / p->temperature;
     a.W = c.W;
-    a.Hc = static_cast<const char*>(c.hidden) + row0 * pl.D * pl.eb;
-    a.tidx_in = c.idx + row0 * pl.K;
+    a.Hc = compact ? hcomp + g * pl.D * pl.eb
+                   : static_cast<const char*>(c.hidden) + row0 * pl.D * pl.eb;
+    a.hidden = c.hidden;
+    a.tidx_in = c.idx;
     a.tidx = reinterpret_cast<int32_t*>(ws + pl.off_tidx) + o * pl.K;
     a.tlogit = c.tlogit;
     a.ignore = c.ignore;
     a.inv_nvalid = inv_nvalid;
+    a.rowmap = compact ? rowmap + g : nullptr;
+    a.nrow = compact ? gnrow : nullptr;
+    a.nrow_base = (int)g;
     a.p = reinterpret_cast<float*>(ws + pl.off_p) + o * pl.K;
     a.rowM = rows + o;
     a.rowH = rows + pl.ng + o;
@@ -347,18 +364,34 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     const int64_t row0 = ci * pl.c;
     const int rcount = (int)std::min<int64_t>(pl.c, pl.N - row0);
     const int64_t slot = ci % pl.G;
+    if (compact && slot == 0) {
+      KdCompactArgs k{};
+      k.dtype = p->dtype;
+      k.D = pl.D;
+      k.ignore = c.ignore;
+      k.row0 = row0;
+      k.rows = (int)std::min<int64_t>(pl.G * pl.c, pl.N - row0);
+      k.hidden = c.hidden;
+      k.hcomp = hcomp;
+      k.rowmap = rowmap;
+      k.nrow = gnrow;
+      k.grad_hidden = want_dh ? c.grad_hidden : nullptr;
+      k.gh_f32 = (p->flags & KD_FLAG_GRAD_HIDDEN_F32) ? 1 : 0;
+      k.loss_per_token = c.lpt;
+      if (kd_launch_compact(&k, c.stream) != 0) return KD_ERR_DEVICE;
+    }
     if (pl.prep_per_group && slot == 0) {
       const int grows = (int)std::min<int64_t>(pl.G * pl.c, pl.N - row0);
-      KdChunkArgs g = chunk_args(row0, grows, 0, KD_STAGE_PREP);
+      KdChunkArgs g = chunk_args(row0, grows, 0, 0, KD_STAGE_PREP);
       if (kd_launch_chunk(&g, c.stream) != 0) return KD_ERR_DEVICE;
     }
-    KdChunkArgs a = chunk_args(row0, rcount, pl.prep_per_group ? slot * pl.c : 0,
+    KdChunkArgs a = chunk_args(row0, rcount, pl.prep_per_group ? slot * pl.c : 0, slot * pl.c,
                                pl.prep_per_group ? KD_STAGE_CHUNK
                                                  : (KD_STAGE_PREP | KD_STAGE_CHUNK));
     a.rowFactor = fac + slot * pl.c;
     a.dZ = (want_dh || want_dw) ? ws + pl.off_dz + slot * pl.c * pl.Vp * pl.eb : nullptr;
     a.ldz = pl.Vp;
-    a.loss_per_token = c.lpt ? c.lpt + row0 : nullptr;
+    a.loss_per_token = c.lpt ? (compact ? c.lpt : c.lpt + row0) : nullptr;
     a.block_partial = lossp + n_partials;
     if (kd_launch_chunk(&a, c.stream) != 0) return KD_ERR_DEVICE;
     n_partials += cdiv(rcount, kLossRows);
@@ -376,8 +409,12 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       h.split = choose_dh_split(cdiv(n, kTile) * pl.td, pl.ksteps);
       h.partial = h.split > 1 ? reinterpret_cast<float*>(ws + pl.off_dhs) : nullptr;
       h.gh_f32 = (p->flags & KD_FLAG_GRAD_HIDDEN_F32) ? 1 : 0;
-      h.gH = static_cast<char*>(c.grad_hidden) + r0 * pl.D * (h.gh_f32 ? 4 : pl.eb);
+      h.gH = compact ? c.grad_hidden
+                     : static_cast<char*>(c.grad_hidden) + r0 * pl.D * (h.gh_f32 ? 4 : pl.eb);
       h.rowscale = scaled ? fac + zrow : nullptr;
+      h.rowmap = compact ? rowmap + zrow : nullptr;
+      h.nrow = compact ? gnrow : nullptr;
+      h.nrow_base = (int)zrow;
       return kd_launch_dh(&h, c.stream) == 0;
     };
     if (want_dh && !pl.dh_per_group && !dh(row0, rcount, slot * pl.c)) return KD_ERR_DEVICE;
@@ -392,13 +429,15 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       d.V = pl.V;
       d.dZ = ws + pl.off_dz;
       d.ldz = pl.Vp;
-      d.Hg = static_cast<const char*>(c.hidden) + row_first * pl.D * pl.eb;
+      d.Hg = compact ? c.hidden : static_cast<const char*>(c.hidden) + row_first * pl.D * pl.eb;
       d.tokens = group_tokens;
       d.Ht = ws + pl.off_ht;
       d.beta = (dw_done || c.accumulate) ? 1 : 0;
       d.gW = c.grad_W;
       d.rowscale = scaled ? fac : nullptr;
       d.partial = pl.off_dwp ? reinterpret_cast<float*>(ws + pl.off_dwp) : nullptr;
+      d.rowmap = compact ? rowmap : nullptr;
+      d.nrow = compact ? gnrow : nullptr;
       if (kd_launch_dw(&d, c.stream) != 0) return KD_ERR_DEVICE;
       dw_done = true;
     }

@@ -73,7 +73,9 @@ __global__ void k_fill_f32(float* p, int64_t n, float v) {
 // Row weight coef = g/tau, g = 1/N_valid times the upstream gradient of the
 // mean (gscale, default 1), or the upstream gradient of the token's own loss
 // (gtok); 0 for ignored rows. With a saved log-normaliser (backward only) the
-// row's log2 Z is set from it. One wave per row.
+// row's log2 Z is set from it. One wave per row. With a rowmap, row r is
+// token rowmap[r], and a row without a token (-1) gets p = 0, index -1 and
+// weight 0.
 //
 // The support is a set; a row that repeats an index is read as the dense
 // teacher row that sums the repeated entries (scatter-add): the first
@@ -94,9 +96,10 @@ __host__ __device__ constexpr int prologue_hash_slots(int K) {
 
 __global__ __launch_bounds__(64) void k_teacher_prologue(
     const int32_t* __restrict__ tidx, int32_t* __restrict__ tidx_out, const float* tlogit,
-    const uint8_t* ignore, int64_t row0, int rows, int K, int V, float inv_tau, int logprobs,
-    const float* inv_nvalid, const float* gscale, const float* gtok, const float* logz_in,
-    float* p_out, float* rowM, float* rowH, float* rowCoef, float* rowCoefM, float* rowL2) {
+    const uint8_t* ignore, int64_t row0, const int* __restrict__ rowmap, int rows, int K, int V,
+    float inv_tau, int logprobs, const float* inv_nvalid, const float* gscale, const float* gtok,
+    const float* logz_in, float* p_out, float* rowM, float* rowH, float* rowCoef,
+    float* rowCoefM, float* rowL2) {
   extern __shared__ __attribute__((aligned(16))) char psm[];
   const int T = prologue_hash_slots(K);
   int* hset = reinterpret_cast<int*>(psm);
@@ -105,9 +108,22 @@ __global__ __launch_bounds__(64) void k_teacher_prologue(
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x;
   if (r >= rows) return;
-  const int64_t t = row0 + r;
+  const int64_t t = rowmap != nullptr ? (int64_t)rowmap[r] : row0 + r;
+  if (t < 0) {
+    for (int k = lane; k < K; k += 64) {
+      p_out[(int64_t)r * K + k] = 0.f;
+      tidx_out[(int64_t)r * K + k] = -1;
+    }
+    if (lane == 0) {
+      rowM[r] = 0.f;
+      rowH[r] = 0.f;
+      rowCoef[r] = 0.f;
+      rowCoefM[r] = 0.f;
+    }
+    return;
+  }
   const float* u = tlogit + t * (int64_t)K;
-  const int32_t* ix = tidx + (int64_t)r * K;
+  const int32_t* ix = tidx + t * (int64_t)K;
   for (int i = lane; i < T; i += 64) hset[i] = -1;
   float mx = 0.f, logs = 0.f, scale = 1.f;
   if (!logprobs) {
@@ -694,14 +710,24 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
     const T* __restrict__ W, const T* __restrict__ Hc, int D, int V, int rows, int TM, int TN,
     float k2, float* __restrict__ part_m, float* __restrict__ part_s, int nVT,
     const uint32_t* __restrict__ hits, const int* __restrict__ hoff, int K, T* dZ, int64_t ldz,
-    float* zhit, const float* __restrict__ rowR, int* rowFlag) {
+    float* zhit, const float* __restrict__ rowR, int* rowFlag, const int* __restrict__ nrow,
+    int nrow_base) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
   const int eb = Elt<T>::bytes;
   const int ld = D * eb;
-  const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  // with ignored tokens left out only the first *nrow - nrow_base rows hold
+  // tokens: a tile of rows past them has nothing to compute, and rows past
+  // them in the last tile read hidden rows of zeros (stored like the others,
+  // with a row factor of 0)
+  int trows = rows;
+  if (nrow != nullptr) {
+    trows = min(rows, __builtin_amdgcn_readfirstlane(*nrow) - nrow_base);
+    if (n0 >= trows) return;
+  }
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, trows - n0);
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
 
@@ -845,16 +871,19 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_dz(
 // logit part never exceeds the row's max y beyond rounding, so 2^(y - R)
 // keeps every term that matters; a tile whose sum of 2^(y - R) exceeds
 // 2^kRefGap falls back to its own max. Also clears the row's fallback flag.
+// Row r is token row0 + r, or rowmap[r] (a row without a token has no valid
+// index after the prologue).
 template <typename T>
-__global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, int D,
+__global__ void k_ref_logit(const T* __restrict__ H, const T* __restrict__ W, int D,
                             const int32_t* __restrict__ tidx, const float* __restrict__ tlogit,
-                            int64_t row0, int rows, int K, int V, float k2, float* rowR,
-                            int* rowFlag) {
+                            int64_t row0, const int* __restrict__ rowmap, int rows, int K, int V,
+                            float k2, float* rowR, int* rowFlag) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
+  const int64_t t = rowmap != nullptr ? (int64_t)rowmap[r] : row0 + r;
   const int32_t* ix = tidx + (int64_t)r * K;
-  const float* tl = tlogit + (row0 + r) * (int64_t)K;
+  const float* tl = tlogit + (t < 0 ? 0 : t) * (int64_t)K;
   float best = -INFINITY;
   int bk = K;
   for (int k = lane; k < K; k += 64) {
@@ -877,7 +906,7 @@ __global__ void k_ref_logit(const T* __restrict__ Hc, const T* __restrict__ W, i
   if (bk < K) {
     // 16-byte pieces of both rows (D is a multiple of 64, rows 16-byte aligned)
     constexpr int VPT = 16 / (int)sizeof(T);
-    const T* h = Hc + (int64_t)r * D;
+    const T* h = H + t * D;
     const T* w = W + (int64_t)ix[bk] * D;
     for (int d = lane * VPT; d < D; d += 64 * VPT) {
       const u32x4_t hv = *reinterpret_cast<const u32x4_t*>(h + d);
@@ -931,7 +960,9 @@ __global__ void k_row_loss(const float* zhit, const float* p, int K, const float
 // max); for a row with such a tile, every run brought to mx; the teacher
 // cells (g/tau)(M q - p) (Eq. 3) in the row's stored scale (0 where the
 // factor is 0, i.e. on ignored rows); and the token's loss (Eq. 2) with a
-// partial per block of kLossRows rows as k_row_loss forms it.
+// partial per block of kLossRows rows as k_row_loss forms it. With a rowmap,
+// row r is token rowmap[r] (loss_per_token is then indexed by token), and a
+// row without a token (-1) only gets a row factor of 0 and a loss of 0.
 template <typename T>
 __global__ __launch_bounds__(256) void k_row_finish(
     const float* __restrict__ part_m, const float* __restrict__ part_s, int nVT,
@@ -939,13 +970,19 @@ __global__ __launch_bounds__(256) void k_row_finish(
     const float* __restrict__ p, const float* __restrict__ zhit, int K, int V, float k2,
     const float* __restrict__ rowM, const float* __restrict__ rowH,
     const float* __restrict__ rowCoef, const float* __restrict__ rowCoefM,
-    const uint8_t* __restrict__ ignore, int64_t row0, int rows, float inv_tau, float* rowL2,
-    float* rowFactor, float* loss_per_token, float* block_partial) {
+    const uint8_t* __restrict__ ignore, int64_t row0, const int* __restrict__ rowmap, int rows,
+    float inv_tau, float* rowL2, float* rowFactor, float* loss_per_token, float* block_partial) {
   __shared__ float red[kLossRows];
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int r = blockIdx.x * kLossRows + wave;
   float l = 0.f;
-  if (r < rows) {
+  const int tok = (rowmap != nullptr && r < rows) ? rowmap[r] : 0;
+  if (r < rows && tok < 0) {
+    if (lane == 0) {
+      rowL2[r] = 0.f;
+      rowFactor[r] = 0.f;
+    }
+  } else if (r < rows) {
     const float* pm = part_m + (int64_t)r * nVT;
     const float* ps = part_s + (int64_t)r * nVT;
     // up to 512 vocabulary tiles: the row's partials are loaded into registers
@@ -1029,9 +1066,9 @@ __global__ __launch_bounds__(256) void k_row_finish(
       }
     }
     c = wave_sum(c);
-    const bool valid = ignore == nullptr || ignore[row0 + r] == 0;
+    const bool valid = rowmap != nullptr || ignore == nullptr || ignore[row0 + r] == 0;
     l = valid ? rowH[r] - c * inv_tau + rowM[r] * L2 * kLn2 : 0.f;
-    if (lane == 0 && loss_per_token) loss_per_token[r] = l;
+    if (lane == 0 && loss_per_token) loss_per_token[rowmap != nullptr ? (int64_t)tok : r] = l;
   }
   if (lane == 0) red[wave] = l;
   __syncthreads();
@@ -1059,20 +1096,25 @@ __global__ __launch_bounds__(kFinThreads) void k_finalize_loss(const float* part
 // -------------------------------------------------------------------- dH ----
 // dH_c[t, d] = sum_v dZ[t, v] W[v, d]: A = dZ (K = vocabulary contiguous),
 // B = W read K-major (rows v, columns d); rows of W past V read as zeros. With
-// split > 1 each split covers a K range and writes fp32 partials.
+// split > 1 each split covers a K range and writes fp32 partials. With a
+// rowmap, dZ row t is grad_hidden row rowmap[t] (-1: none), and only the
+// first *nrow - nrow_base rows hold tokens (tiles past them are skipped).
 template <typename T>
 __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, int64_t ldz,
                                                     const T* __restrict__ W, int V, int rows,
                                                     int D, int TM, int TN, int ks_total,
                                                     int split, void* gH, int gh_f32,
                                                     float* partial,
-                                                    const float* __restrict__ rowscale) {
+                                                    const float* __restrict__ rowscale,
+                                                    const int* __restrict__ rowmap,
+                                                    const int* __restrict__ nrow, int nrow_base) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   const int tiles = TM * TN;
   const int sidx = blockIdx.x / tiles;
   int mt, nt;
   tile_coords(blockIdx.x - sidx * tiles, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
+  if (rowmap != nullptr && m0 >= __builtin_amdgcn_readfirstlane(*nrow) - nrow_base) return;
   const int eb = Elt<T>::bytes;
   const int lda = (int)(ldz * eb), ldb = D * eb;
   const int per = (ks_total + split - 1) / split;
@@ -1086,6 +1128,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const float rsv =
       (rowscale != nullptr && split == 1 && tid < kTile && m0 + tid < rows) ? rowscale[m0 + tid]
                                                                            : 1.f;
+  const int rmv = (rowmap != nullptr && split == 1 && tid < kTile && m0 + tid < rows)
+                      ? rowmap[m0 + tid]
+                      : m0 + tid;
   gemm_tile<T, KcOp, KmOp, 8, true, 3>(
       KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
                KmOp{reinterpret_cast<const char*>(W + n0),
@@ -1094,11 +1139,16 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const int lane = tid & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
   float* rsl = reinterpret_cast<float*>(lds);
-  if (tid < kTile) rsl[tid] = rsv;
+  int* rml = reinterpret_cast<int*>(lds) + kTile;
+  if (tid < kTile) {
+    rsl[tid] = rsv;
+    rml[tid] = rmv;
+  }
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const f32x4_t sc = *reinterpret_cast<const f32x4_t*>(rsl + acc_m(wm, i, lane, 0));
+    const i32x4_t om = *reinterpret_cast<const i32x4_t*>(rml + acc_m(wm, i, lane, 0));
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int d = n0 + acc_n(wn, j, lane);
@@ -1109,10 +1159,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
         if (t < rows) {
           if (split == 1) {
             const float v = acc.v[i][j][r] * sc[r];
+            const int64_t o = om[r];  // the grad_hidden row
+            if (o < 0) continue;
             if (gh_f32)
-              static_cast<float*>(gH)[(int64_t)t * D + d] = v;
+              static_cast<float*>(gH)[o * D + d] = v;
             else
-              static_cast<T*>(gH)[(int64_t)t * D + d] = (T)v;
+              static_cast<T*>(gH)[o * D + d] = (T)v;
           } else
             partial[((int64_t)sidx * rows + t) * D + d] = acc.v[i][j][r];
         }
@@ -1123,17 +1175,23 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
 
 template <typename T>
 __global__ void k_dh_reduce(const float* partial, int split, int64_t n, int D,
-                            const float* __restrict__ rowscale, void* gH, int gh_f32) {
+                            const float* __restrict__ rowscale, void* gH, int gh_f32,
+                            const int* __restrict__ rowmap) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (; i < n; i += stride) {
+    const int64_t t = i / D;
+    // with a rowmap: the grad_hidden row of dZ row t (rows without a token,
+    // whose partials were never written, are skipped)
+    const int64_t o = rowmap != nullptr ? (int64_t)rowmap[t] * D + (i - t * D) : i;
+    if (o < 0) continue;
     float s = 0.f;
     for (int k = 0; k < split; ++k) s += partial[(int64_t)k * n + i];
-    const float v = rowscale ? s * rowscale[i / D] : s;
+    const float v = rowscale ? s * rowscale[t] : s;
     if (gh_f32)
-      static_cast<float*>(gH)[i] = v;
+      static_cast<float*>(gH)[o] = v;
     else
-      static_cast<T*>(gH)[i] = (T)v;
+      static_cast<T*>(gH)[o] = (T)v;
   }
 }
 
@@ -1141,11 +1199,13 @@ __global__ void k_dh_reduce(const float* partial, int split, int64_t n, int D,
 // The group's hidden rows transposed: Ht[d, t] = H[t, d] for t < tokens and 0
 // for tokens <= t < ldt (ldt a multiple of 64), so that the dW contraction
 // reads them with the tokens (its K dimension) contiguous. One 64 x 64 block
-// per workgroup, 16-byte loads and stores on both sides.
+// per workgroup, 16-byte loads and stores on both sides. With a rowmap,
+// column t is hidden row rowmap[t] (-1: zeros).
 template <typename T>
 __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H, int tokens,
                                                          int D, T* __restrict__ Ht, int ldt,
-                                                         const float* __restrict__ rowscale) {
+                                                         const float* __restrict__ rowscale,
+                                                         const int* __restrict__ rowmap) {
   constexpr int VPT = 16 / (int)sizeof(T);      // elements per 16-byte piece
   constexpr int PAD = 4 / (int)sizeof(T);       // one dword of padding per LDS row
   __shared__ T tile[64][64 + PAD];              // [token][feature]
@@ -1156,8 +1216,8 @@ __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H,
     const int q = tid + 256 * u;
     const int row = q / (64 / VPT), c = (q % (64 / VPT)) * VPT;
     u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
-    if (t0 + row < tokens)
-      v = *reinterpret_cast<const u32x4_t*>(H + (int64_t)(t0 + row) * D + d0 + c);
+    const int64_t src = t0 + row >= tokens ? -1 : rowmap != nullptr ? rowmap[t0 + row] : t0 + row;
+    if (src >= 0) v = *reinterpret_cast<const u32x4_t*>(H + src * D + d0 + c);
     T e[VPT];
     __builtin_memcpy(e, &v, 16);
     // a per-token factor of the gradient rows is applied to the hidden rows
@@ -1199,15 +1259,21 @@ __global__ __launch_bounds__(256) void k_transpose_rows(const T* __restrict__ H,
 // slot split q + s; k_dw_fixup then adds the parts to grad_W in a fixed
 // order, so the last round is split times shorter. Without SPLIT every block
 // computes a whole tile (nfull, split and partial unused).
+//
+// With nrow (ignored tokens left out), only the group's first *nrow dZ rows
+// hold tokens: the K range stops there, and the dZ rows past it read as
+// zeros.
 template <typename T, bool SPLIT>
 __global__ __launch_bounds__(kThreads, 1) void k_dw(const T* __restrict__ Ht, int ldt,
                                                     const T* __restrict__ dZ, int64_t ldz,
                                                     int tokens, int V, int D, int TM, int TN,
                                                     int beta, float* __restrict__ gW, int nfull,
-                                                    int split, float* __restrict__ partial) {
+                                                    int split, float* __restrict__ partial,
+                                                    const int* __restrict__ nrow) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   constexpr int KS = kRowB / (int)sizeof(T);
-  const int nks = ldt / KS;
+  if (nrow != nullptr) tokens = min(tokens, __builtin_amdgcn_readfirstlane(*nrow));
+  const int nks = min(ldt / KS, (tokens + KS - 1) / KS);
   const int pid = blockIdx.x;
   int L, ks0 = 0, ks1 = nks, slot = -1;
   if (!SPLIT) {
@@ -1318,6 +1384,69 @@ __global__ __launch_bounds__(256) void k_dw_fixup(const float* __restrict__ part
   *reinterpret_cast<f32x4_t*>(gW + (int64_t)v * D + d) = sum;
 }
 
+// ------------------------------------------------- ignored tokens left out --
+// The tokens of a dW group [row0, row0 + rows) that are not ignored, in
+// order: rowmap[j] = the j-th of them, -1 for j >= their count, *nrow = the
+// count. One workgroup: thread i counts a contiguous run of the mask, an
+// exclusive scan of the counts over the threads gives each run its first
+// slot.
+constexpr int kScanThreads = 1024;
+__global__ __launch_bounds__(kScanThreads) void k_compact_scan(const uint8_t* __restrict__ ignore,
+                                                               int64_t row0, int rows,
+                                                               int* __restrict__ rowmap,
+                                                               int* __restrict__ nrow) {
+  __shared__ int sc[kScanThreads];
+  const int tid = threadIdx.x;
+  const int per = (rows + kScanThreads - 1) / kScanThreads;
+  const int b = min(rows, tid * per), e = min(rows, b + per);
+  const uint8_t* m = ignore + row0;
+  int c = 0;
+  for (int i = b; i < e; ++i) c += m[i] == 0 ? 1 : 0;
+  sc[tid] = c;
+  __syncthreads();
+  // inclusive scan (Hillis-Steele) of the counts
+  for (int o = 1; o < kScanThreads; o <<= 1) {
+    const int add = tid >= o ? sc[tid - o] : 0;
+    __syncthreads();
+    sc[tid] += add;
+    __syncthreads();
+  }
+  int pos = sc[tid] - c;
+  const int total = sc[kScanThreads - 1];
+  for (int i = b; i < e; ++i)
+    if (m[i] == 0) rowmap[pos++] = (int)(row0 + i);
+  for (int j = total + tid; j < rows; j += kScanThreads) rowmap[j] = -1;
+  if (tid == 0) nrow[0] = total;
+}
+
+// Row j of the group: hidden row rowmap[j] copied to hcomp row j (j < *nrow);
+// if token row0 + j is ignored, its grad_hidden row and per-token loss are
+// set to 0 (the rest of the call never writes them). One workgroup per row,
+// 16 bytes per thread and step.
+__global__ __launch_bounds__(256) void k_compact_rows(const char* __restrict__ hidden,
+                                                      int64_t row_bytes, int64_t row0,
+                                                      const uint8_t* __restrict__ ignore,
+                                                      const int* __restrict__ rowmap,
+                                                      const int* __restrict__ nrow,
+                                                      char* __restrict__ hcomp, char* gH,
+                                                      int64_t gh_row_bytes, float* lpt) {
+  const int j = blockIdx.x;
+  const int tid = threadIdx.x;
+  if (j < nrow[0]) {
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(hidden + (int64_t)rowmap[j] * row_bytes);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(hcomp + (int64_t)j * row_bytes);
+    for (int64_t q = tid; q < row_bytes / 16; q += 256) dst[q] = src[q];
+  }
+  const int64_t t = row0 + j;
+  if (ignore[t] != 0) {
+    if (gH != nullptr) {
+      u32x4_t* z = reinterpret_cast<u32x4_t*>(gH + t * gh_row_bytes);
+      for (int64_t q = tid; q < gh_row_bytes / 16; q += 256) z[q] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+    if (lpt != nullptr && tid == 0) lpt[t] = 0.f;
+  }
+}
+
 // ------------------------------------------------------------ index check --
 // flag |= 1 if an index is outside [0, V); |= 2 if a row repeats an index.
 __global__ void k_check_indices(const int32_t* idx, int64_t N, int K, int64_t V, int* flag) {
@@ -1382,12 +1511,13 @@ static inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 namespace {
 enum ProfKind {
   P_COUNT_VALID, P_PROLOGUE, P_BUCKET, P_LOGITS, P_MERGE, P_DZ, P_ROW_LOSS, P_DH, P_DH_REDUCE,
-  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_ROW_FINISH, P_DW_FIXUP, P_NKINDS
+  P_DW, P_FINALIZE, P_FILL, P_TRANSPOSE, P_LOGITS_DZ, P_REF, P_ROW_FINISH, P_DW_FIXUP,
+  P_COMPACT, P_NKINDS
 };
 const char* const kProfNames[P_NKINDS] = {
     "count_valid", "teacher_prologue", "bucket", "logits_lse", "lse_merge", "dz", "row_loss",
     "dh", "dh_reduce", "dw", "finalize_loss", "fill", "transpose_rows", "logits_dz", "ref_logit",
-    "row_finish", "dw_fixup"};
+    "row_finish", "dw_fixup", "compact"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -1488,7 +1618,8 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
       ProfScope ps_(P_PROLOGUE, 0.0, s);
       hipLaunchKernelGGL(k_teacher_prologue, dim3(a.rows), dim3(64),
                          (size_t)4 * prologue_hash_slots(a.K) + (size_t)8 * a.K, s, a.tidx_in,
-                         a.tidx, a.tlogit, a.ignore, a.row0, a.rows, a.K, (int)a.V, a.inv_tau,
+                         a.tidx, a.tlogit, a.ignore, a.row0, a.rowmap, a.rows, a.K, (int)a.V,
+                         a.inv_tau,
                          a.teacher_logprobs, a.inv_nvalid, a.gscale, a.gtok,
                          fwd ? nullptr : a.logz_in, a.p, a.rowM, a.rowH, a.rowCoef, a.rowCoefM,
                          a.rowL2);
@@ -1500,8 +1631,9 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     }
     if (a.one_projection) {
       ProfScope ps_(P_REF, 0.0, s);
-      hipLaunchKernelGGL(k_ref_logit<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, Hc, W, (int)a.D,
-                         a.tidx, a.tlogit, a.row0, a.rows, a.K, (int)a.V, k2, a.rowR, a.rowFlag);
+      hipLaunchKernelGGL(k_ref_logit<T>, dim3(cdiv(a.rows, 4)), dim3(256), 0, s,
+                         static_cast<const T*>(a.hidden), W, (int)a.D, a.tidx, a.tlogit, a.row0,
+                         a.rowmap, a.rows, a.K, (int)a.V, k2, a.rowR, a.rowFlag);
     }
   }
   if (!(a.stages & KD_STAGE_CHUNK)) return (int)hipGetLastError();
@@ -1513,15 +1645,16 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
       ProfScope ps_(P_LOGITS_DZ, gemm_flops, s);
       hipLaunchKernelGGL(k_logits_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
                          (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT, a.hits,
-                         a.hoff, a.K, static_cast<T*>(a.dZ), a.ldz, a.zhit, a.rowR, a.rowFlag);
+                         a.hoff, a.K, static_cast<T*>(a.dZ), a.ldz, a.zhit, a.rowR, a.rowFlag,
+                         a.nrow, a.nrow_base);
     }
     {
       ProfScope ps_(P_ROW_FINISH, 0.0, s);
       hipLaunchKernelGGL(k_row_finish<T>, dim3(cdiv(a.rows, kLossRows)), dim3(64 * kLossRows), 0,
                          s, a.part_m, a.part_s, a.nVT, a.rowFlag, static_cast<T*>(a.dZ), a.ldz,
                          a.tidx, a.p, a.zhit, a.K, (int)a.V, k2, a.rowM, a.rowH, a.rowCoef,
-                         a.rowCoefM, a.ignore, a.row0, a.rows, a.inv_tau, a.rowL2, a.rowFactor,
-                         a.loss_per_token, a.block_partial);
+                         a.rowCoefM, a.ignore, a.row0, a.rowmap, a.rows, a.inv_tau, a.rowL2,
+                         a.rowFactor, a.loss_per_token, a.block_partial);
     }
   } else {
     if (fwd) {
@@ -1573,13 +1706,13 @@ static int launch_dh_impl(const KdDhArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(k_dh<T>, dim3(TM * TN * a.split), dim3(kThreads), 0, s,
                        static_cast<const T*>(a.dZ), a.ldz, static_cast<const T*>(a.W), (int)a.V,
                        rows, (int)a.D, TM, TN, ks, a.split, a.gH, a.gh_f32, a.partial,
-                       a.rowscale);
+                       a.rowscale, a.rowmap, a.nrow, a.nrow_base);
   }
   if (a.split > 1) {
     const int64_t n = (int64_t)rows * a.D;
     ProfScope ps_(P_DH_REDUCE, 0.0, s);
     hipLaunchKernelGGL(k_dh_reduce<T>, dim3(std::min<int64_t>(cdiv(n, 256), 8192)), dim3(256), 0,
-                       s, a.partial, a.split, n, (int)a.D, a.rowscale, a.gH, a.gh_f32);
+                       s, a.partial, a.split, n, (int)a.D, a.rowscale, a.gH, a.gh_f32, a.rowmap);
   }
   return (int)hipGetLastError();
 }
@@ -1597,7 +1730,7 @@ static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
     ProfScope ps_(P_TRANSPOSE, 0.0, s);
     hipLaunchKernelGGL(k_transpose_rows<T>, dim3(ldt / 64, (int)(a.D / 64)), dim3(256), 0, s,
                        static_cast<const T*>(a.Hg), (int)a.tokens, (int)a.D, Ht, ldt,
-                       a.rowscale);
+                       a.rowscale, a.rowmap);
   }
   const int TM = cdiv(a.D, kTile), TN = cdiv(a.V, kTile);
   const int tiles = TM * TN;
@@ -1617,12 +1750,12 @@ static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
       hipLaunchKernelGGL((k_dw<T, true>), dim3(nfull + (tiles - nfull) * split), dim3(kThreads),
                          0, s, static_cast<const T*>(Ht), ldt, static_cast<const T*>(a.dZ), a.ldz,
                          (int)a.tokens, (int)a.V, (int)a.D, TM, TN, a.beta, a.gW, nfull, split,
-                         a.partial);
+                         a.partial, a.nrow);
     else
       hipLaunchKernelGGL((k_dw<T, false>), dim3(tiles), dim3(kThreads), 0, s,
                          static_cast<const T*>(Ht), ldt, static_cast<const T*>(a.dZ), a.ldz,
                          (int)a.tokens, (int)a.V, (int)a.D, TM, TN, a.beta, a.gW, tiles, 1,
-                         (float*)nullptr);
+                         (float*)nullptr, a.nrow);
   }
   if (nfull < tiles) {
     ProfScope ps_(P_DW_FIXUP, 0.0, s);
@@ -1635,6 +1768,23 @@ static int launch_dw_impl(const KdDwArgs& a, hipStream_t s) {
 extern "C" int kd_launch_dw(const KdDwArgs* a, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   return a->dtype == 1 ? launch_dw_impl<__bf16>(*a, s) : launch_dw_impl<float>(*a, s);
+}
+
+extern "C" int kd_launch_compact(const KdCompactArgs* a, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (a->rows <= 0) return 0;
+  const int64_t eb = a->dtype == 1 ? 2 : 4;
+  {
+    ProfScope ps_(P_COMPACT, 0.0, s);
+    hipLaunchKernelGGL(k_compact_scan, dim3(1), dim3(kScanThreads), 0, s, a->ignore, a->row0,
+                       a->rows, a->rowmap, a->nrow);
+    hipLaunchKernelGGL(k_compact_rows, dim3(a->rows), dim3(256), 0, s,
+                       static_cast<const char*>(a->hidden), a->D * eb, a->row0, a->ignore,
+                       a->rowmap, a->nrow, static_cast<char*>(a->hcomp),
+                       static_cast<char*>(a->grad_hidden), a->D * (a->gh_f32 ? 4 : eb),
+                       a->loss_per_token);
+  }
+  return (int)hipGetLastError();
 }
 
 extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {

@@ -44,12 +44,19 @@ struct KdChunkArgs {
   int rows;                 // tokens in the chunk (prepared rows)
   float inv_tau;
   const void* W;            // [V, D]
-  const void* Hc;           // hidden + row0 * D
-  const int32_t* tidx_in;   // teacher_idx + row0 * K (the caller's)
+  const void* Hc;           // hidden + row0 * D (the projection's token rows)
+  const void* hidden;       // full [N, D] (the reference logits read rows by token)
+  const int32_t* tidx_in;   // full [N, K] (the caller's)
   int32_t* tidx;            // [rows, K] the prologue's copy (repeats -1), read by the rest
   const float* tlogit;      // full [N, K] (prologue indexes with row0)
   const uint8_t* ignore;    // full [N] or null
   const float* inv_nvalid;
+  // ignored tokens left out (one-projection schedule): row r of the prepared
+  // rows is token rowmap[r] (-1: no token; such rows come after every token),
+  // and *nrow - nrow_base of the rows hold tokens. Null: row r is token row0 + r.
+  const int* rowmap;
+  const int* nrow;
+  int nrow_base;
   // per-chunk workspace
   float* p;                 // [rows, K]
   float *rowM, *rowH, *rowCoef, *rowCoefM, *rowL2;   // [rows]
@@ -66,7 +73,7 @@ struct KdChunkArgs {
   void* dZ;                 // this chunk's rows of the group's dZ [rows, ldz]
   int64_t ldz;              // = padded vocabulary (columns V..ldz: finite, z = 0 there)
   // outputs
-  float* loss_per_token;    // + row0, or null
+  float* loss_per_token;    // + row0 (full [N] with a rowmap), or null
   float* block_partial;     // this chunk's cdiv(rows, kLossRows) partial sums
 };
 
@@ -80,9 +87,12 @@ struct KdDhArgs {
   int64_t tokens;           // tokens in the group
   int split;                // split of the vocabulary (K) range, >= 1
   float* partial;           // [split, tokens, D] when split > 1
-  void* gH;                 // grad_hidden + the group's first row * D
+  void* gH;                 // grad_hidden + the group's first row * D (full with a rowmap)
   int gh_f32;               // grad_hidden is fp32 (else the operands' dtype)
   const float* rowscale;    // [tokens] factor of each dZ row, or null (= 1)
+  const int* rowmap;        // [tokens] grad_hidden row of each dZ row (-1: none), or null
+  const int* nrow;          // with rowmap: *nrow - nrow_base dZ rows hold tokens
+  int nrow_base;
 };
 
 // dW tiles per full round (the compute units) and the largest split of the
@@ -97,7 +107,7 @@ struct KdDwArgs {
   int64_t D, V;
   const void* dZ;           // the group's dZ rows [tokens, ldz]
   int64_t ldz;
-  const void* Hg;           // the group's hidden rows [tokens, D]
+  const void* Hg;           // the group's hidden rows [tokens, D] (full with a rowmap)
   int64_t tokens;           // tokens in the group
   void* Ht;                 // workspace for Hg transposed: [D, tokens rounded up to 64]
   int beta;                 // 0 overwrite, 1 accumulate
@@ -105,6 +115,27 @@ struct KdDwArgs {
   const float* rowscale;    // [tokens] factor of each dZ row (applied to the
                             // hidden rows), or null (= 1)
   float* partial;           // workspace of the split tail tiles, or null (no split)
+  const int* rowmap;        // [tokens] hidden row of each dZ row (-1: none), or null
+  const int* nrow;          // with rowmap: the dZ rows [0, *nrow) hold tokens
+};
+
+// Ignored tokens of one dW group [row0, row0 + rows) left out: rowmap[j] =
+// the j-th token not ignored (then -1), *nrow = their count, their hidden
+// rows copied to hcomp [rows, D]; the ignored tokens' grad_hidden rows and
+// per-token losses set to 0.
+struct KdCompactArgs {
+  int dtype;
+  int64_t D;
+  const uint8_t* ignore;    // full [N]
+  int64_t row0;
+  int rows;
+  const void* hidden;       // full [N, D]
+  void* hcomp;
+  int* rowmap;
+  int* nrow;
+  void* grad_hidden;        // full [N, D] or null
+  int gh_f32;
+  float* loss_per_token;    // full [N] or null
 };
 
 extern "C" {
@@ -112,6 +143,7 @@ int kd_launch_prepare(const KdPrepareArgs* a, void* stream);
 int kd_launch_chunk(const KdChunkArgs* a, void* stream);
 int kd_launch_dh(const KdDhArgs* a, void* stream);
 int kd_launch_dw(const KdDwArgs* a, void* stream);
+int kd_launch_compact(const KdCompactArgs* a, void* stream);
 int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid, float* loss,
                        void* stream);
 int kd_launch_scale(int out_bf16, const float* x, void* y, int64_t n, const float* g,
