@@ -95,7 +95,7 @@ typedef struct kd_problem {
 /*
  * Bytes of device workspace kd_topk_kl_fwd_bwd, kd_topk_kl_fwd,
  * kd_topk_kl_bwd and kd_topk_kl_check_indices need for problem *p. Pure host
- * function: touches no device. The size is O(N/4 + G C_s (V + K) + D G C_s),
+ * function: touches no device. The size is O(N/4 + G C_s (V + K + 1) + D G C_s),
  * with G C_s <= 16384 the tokens whose dZ rows one grad_W contraction
  * gathers (at most 4 GiB of them), plus 64 MiB when grad_W's tiles leave the
  * last round of the compute units partly filled: it grows with N only
@@ -148,6 +148,15 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  * of Algorithm 1's logit recompute (which the split entry points below
  * keep). The transient [chunk, V] buffer is the same one; nothing of size
  * N x V exists. The stream's device must be the current device.
+ *
+ * With an ignore mask in that schedule, the ignored tokens take no part in
+ * the contractions: their loss terms and gradient rows are 0 (Eq. 3 weights
+ * every row of G by its mask), so each group of up to 16384 tokens is first
+ * compacted to its tokens that are not ignored, the projection, dH and dW
+ * run over those only (the count stays on the device: no host
+ * synchronisation), and the ignored tokens' loss_per_token entries and
+ * grad_hidden rows are written as 0. The results are those of the
+ * uncompacted computation up to the order of fp32 sums.
  *
  * Pointers hidden, W, grad_hidden, grad_W and workspace must be 16-byte
  * aligned (KD_ERR_UNSUPPORTED otherwise). hidden, W, teacher_idx,
