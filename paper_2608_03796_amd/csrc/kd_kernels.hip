@@ -1128,9 +1128,6 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   const float rsv =
       (rowscale != nullptr && split == 1 && tid < kTile && m0 + tid < rows) ? rowscale[m0 + tid]
                                                                            : 1.f;
-  const int rmv = (rowmap != nullptr && split == 1 && tid < kTile && m0 + tid < rows)
-                      ? rowmap[m0 + tid]
-                      : m0 + tid;
   gemm_tile<T, KcOp, KmOp, 8, true, 3>(
       KcOp{reinterpret_cast<const char*>(dZ + (int64_t)m0 * ldz), (uint32_t)(mrows * lda), lda},
                KmOp{reinterpret_cast<const char*>(W + n0),
@@ -1142,7 +1139,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_dh(const T* __restrict__ dZ, in
   int* rml = reinterpret_cast<int*>(lds) + kTile;
   if (tid < kTile) {
     rsl[tid] = rsv;
-    rml[tid] = rmv;
+    // the output row of each of the tile's rows (loaded here: nothing of the
+    // unmasked call is kept live through the main loop for it)
+    rml[tid] = (rowmap != nullptr && split == 1 && m0 + tid < rows) ? rowmap[m0 + tid] : m0 + tid;
   }
   __syncthreads();
 #pragma unroll
@@ -1789,18 +1788,16 @@ extern "C" int kd_launch_compact(const KdCompactArgs* a, void* stream) {
 
 extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-{
+  {
     ProfScope ps_(P_COUNT_VALID, 0.0, s);
-    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(kCountThreads), 0, s, a->ignore, a->N, a->nvalid,
-                     a->inv_nvalid);
-    }
+    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(kCountThreads), 0, s, a->ignore, a->N,
+                       a->nvalid, a->inv_nvalid);
+  }
   if (a->zero_gW != nullptr) {
     const int64_t n = a->V * a->D;
-{
     ProfScope ps_(P_FILL, 0.0, s);
     hipLaunchKernelGGL(k_fill_f32, dim3(std::min<int64_t>(cdiv(n, 256), 16384)), dim3(256), 0, s,
                        a->zero_gW, n, 0.0f);
-    }
   }
   return (int)hipGetLastError();
 }
@@ -1808,11 +1805,11 @@ extern "C" int kd_launch_prepare(const KdPrepareArgs* a, void* stream) {
 extern "C" int kd_launch_finalize(const float* partials, int n, const float* inv_nvalid,
                                   float* loss, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-{
+  {
     ProfScope ps_(P_FINALIZE, 0.0, s);
     hipLaunchKernelGGL(k_finalize_loss, dim3(1), dim3(kFinThreads), 0, s, partials, n, inv_nvalid,
                        loss);
-    }
+  }
   return (int)hipGetLastError();
 }
 
