@@ -457,15 +457,24 @@ def main():
     # two forward passes in one); the fused call runs three (6 N D V), which
     # the library reports per launch and the MFMA fraction is taken on
     equiv_flops = 8.0 * w.N * w.D * w.V
-    executed = sum(v["flops"] for v in prof.values()) / args.steps
+    # With a mask the fused call leaves the ignored tokens out of its
+    # contractions. The library counts each launch's FLOP over all the rows it
+    # is given, so every contraction kind sums to 2 N D V per step; the tokens
+    # that are not ignored make 2 N_valid D V of it, which is what the step
+    # computes for the loss (the hardware also runs the rows that complete a
+    # tile: under 256 per projection or dH launch and 64 per dW launch, which
+    # the MFMA counters show and this leaves out).
+    useful = n_valid / w.N if inp["ignore"] is not None else 1.0
+    executed = sum(v["flops"] for v in prof.values()) / args.steps * useful
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     dom_name, dom = max(prof.items(), key=lambda kv: kv[1]["total_ms"])
-    achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12 if dom["total_ms"] > 0 else 0.0
+    dom_flops = dom["flops"] * useful
+    achieved = dom_flops / (dom["total_ms"] / 1e3) / 1e12 if dom["total_ms"] > 0 else 0.0
     roofline = {"bound": "mfma", "kernel": dom_name, "achieved": round(achieved, 2),
                 "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                 "traffic": stored_traffic(dom_name, w.name),
                 "avg_launch_ms": round(dom["total_ms"] / dom["launches"], 4),
-                "flop_per_launch": dom["flops"] / dom["launches"]}
+                "flop_per_launch": dom_flops / dom["launches"]}
     # every kernel's share of a step, from a second pass with an event pair
     # around every launch (the events' cost is why the timed pass above
     # records them around the contractions only)
@@ -476,7 +485,7 @@ def main():
     kd.profile_enable(False)
     prof_all = kd.profile_read()
     kernels = {k: {"launches": v["launches"], "ms_per_step": round(v["total_ms"] / args.steps, 4),
-                   "tflops": (round(v["flops"] / (v["total_ms"] / 1e3) / 1e12, 2)
+                   "tflops": (round(v["flops"] * useful / (v["total_ms"] / 1e3) / 1e12, 2)
                               if v["flops"] and v["total_ms"] > 0 else None)}
                for k, v in sorted(prof_all.items(), key=lambda kv: -kv[1]["total_ms"])}
     paper = PAPER_TOKENS_PER_S.get(w.name)
@@ -494,10 +503,12 @@ def main():
         "gemm_flop_per_step": executed,
         "mfma_pct_8ndv_equivalent": round(100.0 * equiv_flops / (ms / 1e3) / (peak * 1e12), 2),
         "flop_basis": ("mfma_pct = the FLOP the step's contraction kernels execute "
-                       "(gemm_flop_per_step: one projection per chunk plus dH and dW, 6 N D V) "
+                       "(gemm_flop_per_step: one projection per chunk plus dH and dW, 6 N D V; "
+                       "with a mask 6 N_valid D V, the ignored tokens being left out) "
                        "per second over the dense peak; mfma_pct_8ndv_equivalent counts the "
-                       "metric's 8 N D V per step instead (an equivalent rate, not "
-                       "utilisation: the fused call does not execute the fourth contraction)"),
+                       "metric's 8 N D V per step (all N positions) instead (an equivalent "
+                       "rate, not utilisation: the fused call does not execute the fourth "
+                       "contraction)"),
         "sclk_mhz": round(clk, 1) if clk else None,
         "sclk_samples": len(clock.samples),
         "mfma_pct_at_measured_sclk": (round(100.0 * executed / (ms / 1e3)
