@@ -149,13 +149,13 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  * keep). The transient [chunk, V] buffer is the same one; nothing of size
  * N x V exists. The stream's device must be the current device.
  *
- * With an ignore mask in that schedule, the ignored tokens take no part in
- * the contractions: their loss terms and gradient rows are 0 (Eq. 3 weights
- * every row of G by its mask), so each group of up to 16384 tokens is first
- * compacted to its tokens that are not ignored, the projection, dH and dW
- * run over those only (the count stays on the device: no host
- * synchronisation), and the ignored tokens' loss_per_token entries and
- * grad_hidden rows are written as 0. The results are those of the
+ * With an ignore mask, the ignored tokens take no part in the contractions
+ * (with or without gradients requested): their loss terms and gradient rows
+ * are 0 (Eq. 3 weights every row of G by its mask), so each group of up to
+ * 16384 tokens is first compacted to its tokens that are not ignored, the
+ * projection, dH and dW run over those only (the count stays on the device:
+ * no host synchronisation), and the ignored tokens' loss_per_token entries
+ * and grad_hidden rows are written as 0. The results are those of the
  * uncompacted computation up to the order of fp32 sums.
  *
  * Pointers hidden, W, grad_hidden, grad_W and workspace must be 16-byte

@@ -443,9 +443,11 @@ def _autograd_functions():
             need_h, need_W = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
             ctx.grads = None
             if not (need_h or need_W):
-                return fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
-                           chunk=chunk, teacher_logprobs=teacher_logprobs,
-                           workspace=workspace)["loss"]
+                # the loss alone (no log Z to save): the fused call without
+                # gradients, which leaves ignored tokens out
+                return fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
+                               chunk=chunk, grad_hidden=False, grad_W=False,
+                               teacher_logprobs=teacher_logprobs, workspace=workspace)["loss"]
             out = fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
                           chunk=chunk, grad_hidden=need_h, grad_W=need_W,
                           teacher_logprobs=teacher_logprobs, workspace=workspace,
@@ -495,8 +497,9 @@ def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore
     gradients ([N, D] and [V, D]: 2.5 GiB at N = 32768, D = 4096,
     V = 131072) until the graph is freed; they are kept on the autograd
     context, so saved-tensor hooks (offloading) do not see them. Compute such
-    a loss under torch.no_grad(), or use schedule="recompute", whose forward
-    is kd_topk_kl_fwd alone and which saves only log Z.
+    a loss under torch.no_grad() (the loss alone, through kd_topk_kl_fwd_bwd
+    without gradients), or use schedule="recompute", whose forward is
+    kd_topk_kl_fwd alone and which saves only log Z.
     schedule="recompute": Algorithm 1's schedule through the split entry
     points (forward saves log Z; backward recomputes the logits).
     workspace: a uint8 device tensor of at least workspace_size(...) bytes to
@@ -506,9 +509,11 @@ def topk_kl_loss(hidden, W, teacher_idx, teacher_logit, tau: float = 1.0, ignore
     if schedule not in ("fused", "recompute"):
         raise ValueError("schedule must be 'fused' or 'recompute'")
     if not torch.is_grad_enabled():
-        # no graph will be built: the loss alone (no gradient work)
-        return fwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore, chunk=chunk,
-                   teacher_logprobs=teacher_logprobs, workspace=workspace)["loss"]
+        # no graph will be built: the loss alone (no gradient work; ignored
+        # tokens left out)
+        return fwd_bwd(hidden, W, teacher_idx, teacher_logit, tau=tau, ignore=ignore,
+                       chunk=chunk, grad_hidden=False, grad_W=False,
+                       teacher_logprobs=teacher_logprobs, workspace=workspace)["loss"]
     if _TOPK_KL is None:
         _TOPK_KL = _autograd_functions()
     return _TOPK_KL[schedule].apply(hidden, W, teacher_idx, teacher_logit, float(tau), ignore,

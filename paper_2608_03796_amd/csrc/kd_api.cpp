@@ -301,11 +301,13 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
   // the single-projection schedule stores dZ up to a factor per row, which
   // dH applies to its rows and dW to the hidden rows
   const bool scaled = fwd && bwd && (want_dh || want_dw);
-  // With a mask, that schedule leaves the ignored tokens out (their loss and
+  // With a mask, the fused call leaves the ignored tokens out (their loss and
   // gradient rows are 0): each dW group's other tokens are gathered first,
   // and the group's rows are those tokens in order, then rows without a
   // token, whose tiles the contractions skip (their count is on the device).
-  const bool compact = scaled && c.ignore != nullptr;
+  // The split entry points keep every token (their forward returns log Z for
+  // each).
+  const bool compact = c.mode == KD_MODE_FWD_BWD && c.ignore != nullptr && pl.N > 0;
   int* rowmap = reinterpret_cast<int*>(ws + pl.off_rowmap);
   int* gnrow = reinterpret_cast<int*>(ws + pl.off_misc + 16);
   char* hcomp = ws + pl.off_ht;

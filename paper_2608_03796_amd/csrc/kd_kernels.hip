@@ -237,14 +237,23 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
                                                             float* part_s, int nVT,
                                                             const uint32_t* __restrict__ hits,
                                                             const int* __restrict__ hoff, int K,
-                                                            float* zhit) {
+                                                            float* zhit,
+                                                            const int* __restrict__ nrow,
+                                                            int nrow_base) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
   const int eb = Elt<T>::bytes;
   const int ld = D * eb;
-  const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  // with ignored tokens left out only the first *nrow - nrow_base rows hold
+  // tokens (as in k_logits_dz)
+  int trows = rows;
+  if (nrow != nullptr) {
+    trows = min(rows, __builtin_amdgcn_readfirstlane(*nrow) - nrow_base);
+    if (n0 >= trows) return;
+  }
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, trows - n0);
   AccTile acc;
   gemm_tile<T, KcOp, KcOp, 8, false, 3>(
       KcOp{reinterpret_cast<const char*>(W + (int64_t)m0 * D), (uint32_t)(mrows * ld), ld},
@@ -390,10 +399,15 @@ __global__ __launch_bounds__(kThreads, 1) void k_logits_lse(const T* __restrict_
 // order, one wave per token). L2 = log2 sum_v 2^(z_v log2(e)/tau); a partial
 // is the tile max and the sum of 2^(y - max) over the tile's columns.
 __global__ void k_lse_merge(const float* part_m, const float* part_s, int rows, int nVT,
-                            float* rowL2) {
+                            float* rowL2, const int* __restrict__ rowmap) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave_id();
   if (r >= rows) return;
+  if (rowmap != nullptr && rowmap[r] < 0) {
+    // a row without a token: its partials were never written
+    if (lane == 0) rowL2[r] = 0.f;
+    return;
+  }
   const float* pm = part_m + (int64_t)r * nVT;
   const float* ps = part_s + (int64_t)r * nVT;
   float mx = -INFINITY;
@@ -930,20 +944,23 @@ __global__ void k_ref_logit(const T* __restrict__ H, const T* __restrict__ W, in
 // kLossRows rows in a fixed order, for the deterministic mean.
 __global__ void k_row_loss(const float* zhit, const float* p, int K, const float* rowL2,
                            const float* rowM, const float* rowH, const uint8_t* ignore,
-                           int64_t row0, int rows, float inv_tau, float* loss_per_token,
-                           float* logz_out, float* block_partial) {
+                           int64_t row0, const int* __restrict__ rowmap, int rows, float inv_tau,
+                           float* loss_per_token, float* logz_out, float* block_partial) {
   __shared__ float red[kLossRows];
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int r = blockIdx.x * kLossRows + wave;
   float l = 0.f;
-  if (r < rows) {
+  // with a rowmap, row r is token rowmap[r] (loss_per_token indexed by token;
+  // no log Z output), and a row without a token (-1) has a loss of 0
+  const int tok = (rowmap != nullptr && r < rows) ? rowmap[r] : 0;
+  if (r < rows && tok >= 0) {
     float c = 0.f;
     for (int k = lane; k < K; k += 64) c += p[(int64_t)r * K + k] * zhit[(int64_t)r * K + k];
     c = wave_sum(c);
-    const bool valid = ignore == nullptr || ignore[row0 + r] == 0;
+    const bool valid = rowmap != nullptr || ignore == nullptr || ignore[row0 + r] == 0;
     l = valid ? rowH[r] - c * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
     if (lane == 0) {
-      if (loss_per_token) loss_per_token[r] = l;
+      if (loss_per_token) loss_per_token[rowmap != nullptr ? (int64_t)tok : r] = l;
       if (logz_out) logz_out[r] = rowL2[r] * kLn2;
     }
   }
@@ -1663,12 +1680,12 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
         // gradients): z at the teacher entries comes from this GEMM
         hipLaunchKernelGGL(k_logits_lse<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc,
                            (int)a.D, (int)a.V, a.rows, TMv, TNt, k2, a.part_m, a.part_s, a.nVT,
-                           a.hits, a.hoff, a.K, a.zhit);
+                           a.hits, a.hoff, a.K, a.zhit, a.nrow, a.nrow_base);
       }
       {
         ProfScope ps_(P_MERGE, 0.0, s);
         hipLaunchKernelGGL(k_lse_merge, dim3(cdiv(a.rows, 4)), dim3(256), 0, s, a.part_m,
-                           a.part_s, a.rows, a.nVT, a.rowL2);
+                           a.part_s, a.rows, a.nVT, a.rowL2, a.rowmap);
       }
     }
     if (bwd && !fwd) {
@@ -1683,8 +1700,8 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
     if (fwd) {
       ProfScope ps_(P_ROW_LOSS, 0.0, s);
       hipLaunchKernelGGL(k_row_loss, dim3(cdiv(a.rows, kLossRows)), dim3(64 * kLossRows), 0, s,
-                         a.zhit, a.p, a.K, a.rowL2, a.rowM, a.rowH, a.ignore, a.row0, a.rows,
-                         a.inv_tau, a.loss_per_token, a.logz_out, a.block_partial);
+                         a.zhit, a.p, a.K, a.rowL2, a.rowM, a.rowH, a.ignore, a.row0, a.rowmap,
+                         a.rows, a.inv_tau, a.loss_per_token, a.logz_out, a.block_partial);
     }
   }
   return (int)hipGetLastError();

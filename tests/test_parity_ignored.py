@@ -73,6 +73,13 @@ CASES = [
     ("logprobs", 600, 64, 4096, 37, 128, "bf16", "p30", 1.0, {"logprobs": True}),
     ("frozen_W", 600, 64, 4096, 16, 128, "bf16", "half", 1.0, {"grad_W": False}),
     ("no_grad_hidden", 600, 64, 4096, 16, 128, "bf16", "half", 1.0, {"grad_hidden": False}),
+    ("mask_at_odd_address", 1000, 128, 5003, 16, 256, "bf16", "half", 1.0, {"mask_offset": 3}),
+    ("loss_only", 1000, 128, 5003, 16, 256, "bf16", "half", 1.0,
+     {"grad_hidden": False, "grad_W": False}),
+    ("loss_only_f32_groups", 40000, 64, 1000, 8, 4096, "f32", "groups", 1.0,
+     {"grad_hidden": False, "grad_W": False}),
+    ("loss_only_all_ignored", 300, 64, 1000, 8, 100, "bf16", "all", 1.0,
+     {"grad_hidden": False, "grad_W": False}),
 ]
 
 
@@ -96,6 +103,13 @@ def test_ignored_tokens(gpu_lib, case):
     if logprobs:
         logit = (torch.log_softmax(logit, dim=1) - 0.2).contiguous()
     ignore = _mask(N, mkind, ki.SEED_MASK + seed).to(dev)
+    if ex.get("mask_offset"):
+        # a mask that starts at an address that is not 4-byte aligned
+        o = ex["mask_offset"]
+        buf = torch.zeros(N + o, dtype=torch.uint8, device=dev)
+        buf[o:] = ignore
+        ignore = buf[o:]
+        assert ignore.data_ptr() % 4 == o % 4
     want_h, want_W = ex.get("grad_hidden", True), ex.get("grad_W", True)
     gh_f32 = ex.get("gh_f32", False)
     acc = ex.get("accumulate", False)

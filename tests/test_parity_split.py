@@ -54,9 +54,14 @@ def test_forward_matches_fused_and_oracle(gpu_lib, dtype, N, D, V, K, chunk, tau
     fb = kd.fwd_bwd(*_args(inp), tau=tau, ignore=inp["ignore"], chunk=chunk, loss_per_token=True,
                     grad_hidden=False, grad_W=False)
     torch.cuda.synchronize()
-    # the same kernels compute the loss in both entry points
-    assert torch.equal(f["loss"], fb["loss"])
+    # the same kernels compute each token's loss in both entry points; with a
+    # mask the fused call leaves the ignored tokens out, so its partial sums
+    # group the tokens differently (same terms, another fp32 order)
     assert torch.equal(f["loss_per_token"], fb["loss_per_token"])
+    if inp["ignore"] is None:
+        assert torch.equal(f["loss"], fb["loss"])
+    else:
+        assert abs(float(f["loss"]) - float(fb["loss"])) <= 1e-6 * abs(float(f["loss"]))
     ref = kd_topk_kl(**oracle_inputs(inp), tau=tau, chunk=chunk, want_grads=False)
     tol = TOL[dtype]
     assert abs(float(f["loss"]) - ref["loss"]) <= tol["loss"] * abs(ref["loss"])
