@@ -204,3 +204,33 @@ def test_ignored_tokens_noalloc(gpu_lib):
     torch.cuda.synchronize()
     for k in ("loss", "loss_per_token", "grad_hidden", "grad_W"):
         assert torch.equal(a[k].float(), b[k].float()), k
+
+
+def test_ignored_tokens_noalloc_smaller_groups(gpu_lib):
+    """At V = 131072 the allocation-free call's 256 MiB scratch holds the dZ
+    rows of one 512-token chunk, so its dW groups (and the gathers) are 512
+    tokens where kd_topk_kl_fwd_bwd gathers 4096: both against the oracle."""
+    kd = gpu_lib
+    N, D, V, K, chunk = 4096, 64, 131072, 16, 512
+    print(f"[ignored] noalloc, smaller groups: N={N} D={D} V={V} chunk={chunk}", flush=True)
+    dev = "cuda"
+    h = ki.make_hidden(N, D, torch.bfloat16, dev, seed=ki.SEED_HIDDEN + 800)
+    W = ki.make_weight(V, D, torch.bfloat16, dev, seed=ki.SEED_W + 800, std=0.05)
+    idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + 800)
+    ignore = _mask(N, "half", ki.SEED_MASK + 800).to(dev)
+    a = kd.fwd_bwd(h, W, idx, logit, ignore=ignore, chunk=chunk, loss_per_token=True)
+    b = kd.fwd_bwd_noalloc(h, W, idx, logit, ignore=ignore, chunk=chunk, loss_per_token=True)
+    torch.cuda.synchronize()
+    inp = dict(hidden=h, W=W, teacher_idx=idx, teacher_logit=logit, ignore=ignore)
+    ref = kd_topk_kl(**oracle_inputs(inp), tau=1.0, chunk=chunk)
+    tol = TOL["bf16"]
+    ign = ignore.cpu().numpy().astype(bool)
+    for res in (a, b):
+        assert abs(float(res["loss"]) - ref["loss"]) <= tol["loss"] * abs(ref["loss"])
+        lpt, gh = to64(res["loss_per_token"]), to64(res["grad_hidden"])
+        assert np.all(lpt[ign] == 0.0) and np.all(gh[ign] == 0.0)
+        assert rel_max(lpt, ref["loss_per_token"]) <= tol["loss"]
+        assert rel_max(gh, ref["grad_hidden"]) <= tol["grad"]
+        assert rel_max(to64(res["grad_W"]), ref["grad_W"]) <= tol["grad"]
+    # each token's loss and grad_hidden row come from the same tiles either way
+    assert torch.equal(a["loss_per_token"], b["loss_per_token"])
