@@ -150,7 +150,8 @@ kd_status kd_topk_kl_workspace_size(const kd_problem* p, size_t* bytes);
  * N x V exists. The stream's device must be the current device.
  *
  * With an ignore mask, the ignored tokens take no part in the contractions
- * (with or without gradients requested): their loss terms and gradient rows
+ * (with or without gradients requested, and likewise in kd_topk_kl_fwd and
+ * kd_topk_kl_bwd): their loss terms and gradient rows
  * are 0 (Eq. 3 weights every row of G by its mask), so each group of up to
  * 16384 tokens is first compacted to its tokens that are not ignored, the
  * projection, dH and dW run over those only (the count stays on the device:
@@ -188,12 +189,14 @@ kd_status kd_topk_kl_fwd_bwd(const kd_problem* p,
  *   loss          [1] fp32            out: mean of l_t over non-ignored tokens
  *   loss_per_token [N] fp32 or NULL   out: l_t (0 on ignored tokens)
  *   saved_logz    [N] fp32            out: log Z_t = logsumexp_v z_tv / tau
+ *                                     (0 on ignored tokens, which are left
+ *                                     out as in kd_topk_kl_fwd_bwd)
  *   workspace, workspace_bytes, hip_stream   as for kd_topk_kl_fwd_bwd
  *
  * One projection per chunk (the normaliser and the student logits at the
  * teacher entries come from the same tile). Values are bitwise identical to
- * the corresponding outputs of kd_topk_kl_fwd_bwd. Errors as for
- * kd_topk_kl_fwd_bwd; saved_logz is required.
+ * the corresponding outputs of kd_topk_kl_fwd_bwd called without gradients.
+ * Errors as for kd_topk_kl_fwd_bwd; saved_logz is required.
  */
 kd_status kd_topk_kl_fwd(const kd_problem* p,
                          const void* hidden,
@@ -214,7 +217,8 @@ kd_status kd_topk_kl_fwd(const kd_problem* p,
  * grad_hidden = G W and grad_W (+)= G^T h).
  *
  *   hidden, W, teacher_idx, teacher_logit, ignore   as for the forward call
- *   saved_logz    [N] fp32            log Z_t written by kd_topk_kl_fwd
+ *   saved_logz    [N] fp32            log Z_t written by kd_topk_kl_fwd (read
+ *                                     for the tokens not ignored)
  *   grad_loss     [1] fp32 or NULL    upstream gradient of the mean loss
  *                                     (device scalar); NULL = 1
  *   grad_loss_per_token [N] fp32 or NULL   upstream gradients u_t of the

@@ -301,13 +301,12 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
   // the single-projection schedule stores dZ up to a factor per row, which
   // dH applies to its rows and dW to the hidden rows
   const bool scaled = fwd && bwd && (want_dh || want_dw);
-  // With a mask, the fused call leaves the ignored tokens out (their loss and
-  // gradient rows are 0): each dW group's other tokens are gathered first,
-  // and the group's rows are those tokens in order, then rows without a
-  // token, whose tiles the contractions skip (their count is on the device).
-  // The split entry points keep every token (their forward returns log Z for
-  // each).
-  const bool compact = c.mode == KD_MODE_FWD_BWD && c.ignore != nullptr && pl.N > 0;
+  // With a mask, every entry point leaves the ignored tokens out (their loss
+  // and gradient rows are 0): each dW group's other tokens are gathered
+  // first, and the group's rows are those tokens in order, then rows without
+  // a token, whose tiles the contractions skip (their count is on the
+  // device).
+  const bool compact = c.ignore != nullptr && pl.N > 0;
   int* rowmap = reinterpret_cast<int*>(ws + pl.off_rowmap);
   int* gnrow = reinterpret_cast<int*>(ws + pl.off_misc + 16);
   char* hcomp = ws + pl.off_ht;
@@ -326,7 +325,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
     a.gscale = c.gscale;
     a.gtok = c.gtok;
     a.logz_in = c.logz_in;
-    a.logz_out = c.logz_out ? c.logz_out + row0 : nullptr;
+    a.logz_out = c.logz_out ? (compact ? c.logz_out : c.logz_out + row0) : nullptr;
     a.D = pl.D;
     a.V = pl.V;
     a.K = (int)pl.K;
@@ -380,6 +379,7 @@ kd_status enqueue(const kd_problem* p, const Plan& pl, const Call& c) {
       k.grad_hidden = want_dh ? c.grad_hidden : nullptr;
       k.gh_f32 = (p->flags & KD_FLAG_GRAD_HIDDEN_F32) ? 1 : 0;
       k.loss_per_token = c.lpt;
+      k.logz_out = c.logz_out;
       if (kd_launch_compact(&k, c.stream) != 0) return KD_ERR_DEVICE;
     }
     if (pl.prep_per_group && slot == 0) {

@@ -119,6 +119,7 @@ __global__ __launch_bounds__(64) void k_teacher_prologue(
       rowH[r] = 0.f;
       rowCoef[r] = 0.f;
       rowCoefM[r] = 0.f;
+      if (logz_in != nullptr) rowL2[r] = 0.f;
     }
     return;
   }
@@ -554,14 +555,21 @@ __global__ __launch_bounds__(kThreads, 1) void k_dz(
     float k2, const float* __restrict__ rowL2, const float* __restrict__ rowCoef,
     const float* __restrict__ rowCoefM, const uint32_t* __restrict__ hits,
     const float* __restrict__ hitp, const int* __restrict__ hoff, int K, int nVT, T* dZ,
-    int64_t ldz, float* zhit) {
+    int64_t ldz, float* zhit, const int* __restrict__ nrow, int nrow_base) {
   __shared__ __attribute__((aligned(16))) char lds[kLdsA3];
   int mt, nt;
   tile_coords(blockIdx.x, TM, TN, 4, mt, nt);
   const int m0 = mt * kTile, n0 = nt * kTile;
   const int eb = Elt<T>::bytes;
   const int ld = D * eb;
-  const int mrows = min(kTile, V - m0), nrows = min(kTile, rows - n0);
+  // with ignored tokens left out only the first *nrow - nrow_base rows hold
+  // tokens (as in k_logits_dz; the rows past them have weight 0)
+  int trows = rows;
+  if (nrow != nullptr) {
+    trows = min(rows, __builtin_amdgcn_readfirstlane(*nrow) - nrow_base);
+    if (n0 >= trows) return;
+  }
+  const int mrows = min(kTile, V - m0), nrows = min(kTile, trows - n0);
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int wm = wave >> 2, wn = wave & 3;
 
@@ -950,8 +958,8 @@ __global__ void k_row_loss(const float* zhit, const float* p, int K, const float
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int r = blockIdx.x * kLossRows + wave;
   float l = 0.f;
-  // with a rowmap, row r is token rowmap[r] (loss_per_token indexed by token;
-  // no log Z output), and a row without a token (-1) has a loss of 0
+  // with a rowmap, row r is token rowmap[r] (loss_per_token and logz_out
+  // indexed by token), and a row without a token (-1) has a loss of 0
   const int tok = (rowmap != nullptr && r < rows) ? rowmap[r] : 0;
   if (r < rows && tok >= 0) {
     float c = 0.f;
@@ -961,7 +969,7 @@ __global__ void k_row_loss(const float* zhit, const float* p, int K, const float
     l = valid ? rowH[r] - c * inv_tau + rowM[r] * rowL2[r] * kLn2 : 0.f;
     if (lane == 0) {
       if (loss_per_token) loss_per_token[rowmap != nullptr ? (int64_t)tok : r] = l;
-      if (logz_out) logz_out[r] = rowL2[r] * kLn2;
+      if (logz_out) logz_out[rowmap != nullptr ? (int64_t)tok : r] = rowL2[r] * kLn2;
     }
   }
   if (lane == 0) red[wave] = l;
@@ -1436,8 +1444,8 @@ __global__ __launch_bounds__(kScanThreads) void k_compact_scan(const uint8_t* __
 }
 
 // Row j of the group: hidden row rowmap[j] copied to hcomp row j (j < *nrow);
-// if token row0 + j is ignored, its grad_hidden row and per-token loss are
-// set to 0 (the rest of the call never writes them). One workgroup per row,
+// if token row0 + j is ignored, its grad_hidden row, per-token loss and saved
+// log Z are set to 0 (the rest of the call never writes them). One workgroup per row,
 // 16 bytes per thread and step.
 __global__ __launch_bounds__(256) void k_compact_rows(const char* __restrict__ hidden,
                                                       int64_t row_bytes, int64_t row0,
@@ -1445,7 +1453,8 @@ __global__ __launch_bounds__(256) void k_compact_rows(const char* __restrict__ h
                                                       const int* __restrict__ rowmap,
                                                       const int* __restrict__ nrow,
                                                       char* __restrict__ hcomp, char* gH,
-                                                      int64_t gh_row_bytes, float* lpt) {
+                                                      int64_t gh_row_bytes, float* lpt,
+                                                      float* logz) {
   const int j = blockIdx.x;
   const int tid = threadIdx.x;
   if (j < nrow[0]) {
@@ -1459,7 +1468,10 @@ __global__ __launch_bounds__(256) void k_compact_rows(const char* __restrict__ h
       u32x4_t* z = reinterpret_cast<u32x4_t*>(gH + t * gh_row_bytes);
       for (int64_t q = tid; q < gh_row_bytes / 16; q += 256) z[q] = u32x4_t{0u, 0u, 0u, 0u};
     }
-    if (lpt != nullptr && tid == 0) lpt[t] = 0.f;
+    if (tid == 0) {
+      if (lpt != nullptr) lpt[t] = 0.f;
+      if (logz != nullptr) logz[t] = 0.f;
+    }
   }
 }
 
@@ -1695,7 +1707,7 @@ static int launch_chunk_impl(const KdChunkArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(k_dz<T>, dim3(TMv * TNt), dim3(kThreads), 0, s, W, Hc, (int)a.D,
                          (int)a.V, a.rows, TMv, TNt, k2, a.rowL2, a.rowCoef, a.rowCoefM, a.hits,
                          a.hitp, a.hoff, a.K, a.nVT, static_cast<T*>(a.dZ), a.ldz,
-                         (float*)nullptr);
+                         (float*)nullptr, a.nrow, a.nrow_base);
     }
     if (fwd) {
       ProfScope ps_(P_ROW_LOSS, 0.0, s);
@@ -1798,7 +1810,7 @@ extern "C" int kd_launch_compact(const KdCompactArgs* a, void* stream) {
                        static_cast<const char*>(a->hidden), a->D * eb, a->row0, a->ignore,
                        a->rowmap, a->nrow, static_cast<char*>(a->hcomp),
                        static_cast<char*>(a->grad_hidden), a->D * (a->gh_f32 ? 4 : eb),
-                       a->loss_per_token);
+                       a->loss_per_token, a->logz_out);
   }
   return (int)hipGetLastError();
 }

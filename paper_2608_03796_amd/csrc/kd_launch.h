@@ -37,7 +37,8 @@ struct KdChunkArgs {
   const float* gscale;      // upstream gradient of the mean (device scalar) or null = 1
   const float* gtok;        // full [N] upstream per-token gradients or null
   const float* logz_in;     // full [N] saved log Z (backward only) or null
-  float* logz_out;          // this chunk's rows of the saved log Z (forward) or null
+  float* logz_out;          // this chunk's rows of the saved log Z (forward; full [N]
+                            // with a rowmap) or null
   int64_t D, V;
   int K;
   int64_t row0;             // first token of the chunk (of the prepared rows)
@@ -121,8 +122,8 @@ struct KdDwArgs {
 
 // Ignored tokens of one dW group [row0, row0 + rows) left out: rowmap[j] =
 // the j-th token not ignored (then -1), *nrow = their count, their hidden
-// rows copied to hcomp [rows, D]; the ignored tokens' grad_hidden rows and
-// per-token losses set to 0.
+// rows copied to hcomp [rows, D]; the ignored tokens' grad_hidden rows,
+// per-token losses and saved log Z set to 0.
 struct KdCompactArgs {
   int dtype;
   int64_t D;
@@ -136,6 +137,7 @@ struct KdCompactArgs {
   void* grad_hidden;        // full [N, D] or null
   int gh_f32;
   float* loss_per_token;    // full [N] or null
+  float* logz_out;          // full [N] or null
 };
 
 extern "C" {
