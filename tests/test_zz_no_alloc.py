@@ -78,7 +78,9 @@ def test_noalloc_call_in_a_graph(gpu_lib):
     """The allocation-free call captured into a HIP graph (torch.cuda.graph) and
     replayed three times, with other eager work (a call through the workspace
     entry point on other inputs, and fills of the outputs) between the replays:
-    every replay rewrites every output bitwise equal to the eager call's."""
+    every replay rewrites every output bitwise equal to the eager call's. A
+    tenth of the tokens is ignored, so the captured call includes the gather
+    of the tokens that are not ignored and the skip of the tiles past them."""
     kd = gpu_lib
     N, D, V, K, chunk, tau = 1000, 256, 50000, 32, 256, 1.5
     dev = "cuda"
@@ -86,24 +88,28 @@ def test_noalloc_call_in_a_graph(gpu_lib):
     W = ki.make_weight(V, D, torch.bfloat16, dev, seed=ki.SEED_W + 61)
     idx, logit = ki.make_teacher(N, K, V, dev, seed=ki.SEED_TEACHER + 61)
     h2 = ki.make_hidden(N, D, torch.bfloat16, dev, seed=ki.SEED_HIDDEN + 62)
+    gm = torch.Generator(device="cpu")
+    gm.manual_seed(ki.SEED_MASK + 61)
+    ign = (torch.rand(N, generator=gm) < 0.1).to(torch.uint8).to(dev)
 
     def outs():
         return {"loss": torch.empty((), dtype=torch.float32, device=dev),
                 "loss_per_token": torch.empty(N, dtype=torch.float32, device=dev),
                 "grad_hidden": torch.empty(N, D, dtype=torch.bfloat16, device=dev),
                 "grad_W": torch.empty(V, D, dtype=torch.float32, device=dev)}
-    eager = kd.fwd_bwd_noalloc(h, W, idx, logit, tau=tau, chunk=chunk, out=outs(),
+    eager = kd.fwd_bwd_noalloc(h, W, idx, logit, tau=tau, ignore=ign, chunk=chunk, out=outs(),
                                loss_per_token=True)
     torch.cuda.synchronize()
     out = outs()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        kd.fwd_bwd_noalloc(h, W, idx, logit, tau=tau, chunk=chunk, out=out, loss_per_token=True)
+        kd.fwd_bwd_noalloc(h, W, idx, logit, tau=tau, ignore=ign, chunk=chunk, out=out,
+                           loss_per_token=True)
     torch.cuda.synchronize()
     for rep in range(3):
         for t in out.values():
             t.fill_(float("nan"))
-        other = kd.fwd_bwd(h2, W, idx, logit, tau=tau, chunk=chunk)
+        other = kd.fwd_bwd(h2, W, idx, logit, tau=tau, ignore=ign, chunk=chunk)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
