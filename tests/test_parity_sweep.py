@@ -8,7 +8,8 @@ more than 256 grad_W tiles with a partly filled last round, which the dW
 contraction splits along the tokens), chunks that are ragged, larger than N,
 or multiples of 256 (which the schedule may merge per dW group), temperatures
 0.5 to 2.5, fp32 and bf16, logits and log-probability teachers, 0 to 30% of
-the tokens ignored. Each case prints its configuration before it runs.
+the tokens ignored, then sixteen more with half to all of the tokens ignored.
+Each case prints its configuration before it runs.
 """
 import numpy as np
 import pytest
@@ -21,7 +22,7 @@ from tests.helpers import TOL, oracle_inputs, rel_max, to64
 pytestmark = pytest.mark.gpu
 
 
-def _configs(n=24, seed=2024):
+def _configs(n=24, seed=2024, n_masked=16, seed_masked=2025):
     rng = np.random.default_rng(seed)
     out = []
     for i in range(n):
@@ -36,6 +37,20 @@ def _configs(n=24, seed=2024):
         logprobs = bool(rng.random() < 0.25)
         ign = float(rng.choice([0.0, 0.1, 0.3]))
         out.append((i, N, D, V, K, chunk, tau, dtype, logprobs, ign))
+    # heavier masks (every entry point leaves ignored tokens out), up to all
+    # tokens ignored
+    rng = np.random.default_rng(seed_masked)
+    for i in range(n_masked):
+        N = int(rng.choice([2, 65, 256, 300, 513, 700, 1200]))
+        D = int(rng.choice([64, 128, 256]))
+        K = int(rng.choice([1, 8, 16, 50]))
+        V = max(K, int(rng.choice([300, 997, 4096, 9000])))
+        chunk = int(rng.choice([1, 33, 100, 128, 256, N + 1]))
+        tau = float(np.round(rng.uniform(0.5, 2.5), 2))
+        dtype = "bf16" if rng.random() < 0.5 else "f32"
+        logprobs = bool(rng.random() < 0.25)
+        ign = float(rng.choice([0.5, 0.8, 0.97, 1.0]))
+        out.append((100 + i, N, D, V, K, chunk, tau, dtype, logprobs, ign))
     # more than 256 grad_W tiles with a partly filled last round (split along
     # the tokens), in fp32 and in bf16 with a chunk the schedule merges
     out.append((n, 300, 64, 70000, 16, 100, 1.0, "f32", False, 0.1))
