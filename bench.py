@@ -475,6 +475,11 @@ def main():
                 "traffic": stored_traffic(dom_name, w.name),
                 "avg_launch_ms": round(dom["total_ms"] / dom["launches"], 4),
                 "flop_per_launch": dom_flops / dom["launches"]}
+    # achieved HBM-side rate of the dominant kernel: the counters' bytes per
+    # launch over this run's launch time
+    roofline["traffic_gb_per_s"] = (
+        round(roofline["traffic"] / (roofline["avg_launch_ms"] / 1e3) / 1e9, 1)
+        if roofline["traffic"] else None)
     # every kernel's share of a step, from a second pass with an event pair
     # around every launch (the events' cost is why the timed pass above
     # records them around the contractions only)
