@@ -1,6 +1,10 @@
 // HIP kernels (gfx950) of the fused chunked top-K KL loss and their launchers.
 //
 // Per call:    count_valid
+// Per group of chunks, with a mask:
+//              compact_scan, compact_rows -> the group's tokens that are not
+//                                   ignored (row map, count, their hidden rows);
+//                                   the kernels below then skip the rows past them
 // Per chunk:   teacher_prologue  -> p, M, H, g/tau                 (§3.2, Eq. 2 terms)
 //              bucket            -> teacher entries grouped by vocabulary tile
 //   loss and gradients together (one projection per chunk):
