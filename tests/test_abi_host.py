@@ -26,7 +26,8 @@ def lib():
 
 
 def test_exports_every_declared_symbol(lib):
-    text = open(HEADER).read()
+    with open(HEADER) as f:
+        text = f.read()
     declared = set(re.findall(r"^\s*(?:kd_status|const char\*|int)\s+(kd_\w+)\s*\(", text, re.M))
     assert declared == set(kd.EXPORTED)
     for name in declared:
@@ -34,7 +35,8 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    text = open(HEADER).read()
+    with open(HEADER) as f:
+        text = f.read()
     v = int(re.search(r"#define KDTOPK_ABI_VERSION (\d+)", text).group(1))
     assert lib.kd_abi_version() == v
 

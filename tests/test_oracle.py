@@ -180,7 +180,7 @@ def test_autograd_of_dense_textbook_loss(tau):
     per = torch.nn.functional.kl_div(logq, P, reduction="none").sum(dim=1)
     loss = (per * valid).sum() / valid.sum()
     loss.backward()
-    assert out["loss"] == pytest.approx(float(loss), rel=1e-12)
+    assert out["loss"] == pytest.approx(float(loss.detach()), rel=1e-12)
     np.testing.assert_allclose(out["grad_hidden"], th.grad.numpy(), rtol=1e-10, atol=1e-14)
     np.testing.assert_allclose(out["grad_W"], tW.grad.numpy(), rtol=1e-10, atol=1e-14)
 

@@ -108,7 +108,7 @@ def test_partial_mass_autograd(tau):
     per = (P * (torch.where(P > 0, torch.log(P), torch.zeros_like(P)) - logq)).sum(dim=1)
     loss = per.mean()
     loss.backward()
-    assert out["loss"] == pytest.approx(float(loss), rel=1e-12)
+    assert out["loss"] == pytest.approx(float(loss.detach()), rel=1e-12)
     np.testing.assert_allclose(out["grad_hidden"], th.grad.numpy(), rtol=1e-10, atol=1e-13)
     np.testing.assert_allclose(out["grad_W"], tW.grad.numpy(), rtol=1e-10, atol=1e-13)
 

@@ -44,7 +44,8 @@ MUTATIONS = {
 
 
 def _load_mutant(old, new):
-    src = open(ORACLE_SRC).read()
+    with open(ORACLE_SRC) as f:
+        src = f.read()
     assert old in src, old
     mod = types.ModuleType("kd_oracle_mutant")
     exec(compile(src.replace(old, new, 1), "kd_oracle_mutant", "exec"), mod.__dict__)
@@ -55,7 +56,9 @@ def _pins(fn):
     """Returns the names of the pins that fail for oracle function `fn`."""
     failed = []
     # golden hand-derived cases
-    for case in json.load(open(GOLDEN))["cases"]:
+    with open(GOLDEN) as f:
+        cases = json.load(f)["cases"]
+    for case in cases:
         ign = None if case["ignore"] is None else np.array(case["ignore"], dtype=np.uint8)
         try:
             out = fn(np.array(case["h"]), np.array(case["W"]), np.array(case["teacher_idx"]),
