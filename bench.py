@@ -71,13 +71,45 @@ def sclk_mhz():
     return None
 
 
+def _hwmon_files(name):
+    import glob
+    return sorted(glob.glob(f"/sys/class/drm/card*/device/hwmon/hwmon*/{name}"))
+
+
+def power_w():
+    """Board power from the driver's hwmon (average, else instantaneous), in
+    watts (None if unreadable)."""
+    for name in ("power1_average", "power1_input"):
+        for f in _hwmon_files(name):
+            try:
+                with open(f) as fh:
+                    v = float(fh.read().strip()) / 1e6
+                if v > 0:
+                    return v
+            except (OSError, ValueError):
+                continue
+    return None
+
+
+def power_cap_w():
+    """The board power cap the driver enforces, in watts (None if unreadable)."""
+    for f in _hwmon_files("power1_cap"):
+        try:
+            with open(f) as fh:
+                return float(fh.read().strip()) / 1e6
+        except (OSError, ValueError):
+            continue
+    return None
+
+
 class ClockSampler:
-    """Samples the shader clock every `period` seconds on a background thread
-    (the main thread sits in a blocking device synchronise meanwhile)."""
+    """Samples the shader clock (and the board power) every `period` seconds
+    on a background thread (the main thread sits in a blocking device
+    synchronise meanwhile)."""
 
     def __init__(self, period=0.02):
         import threading
-        self.period, self.samples = period, []
+        self.period, self.samples, self.power = period, [], []
         self._stop = threading.Event()
         self._t = threading.Thread(target=self._run, daemon=True)
 
@@ -86,6 +118,9 @@ class ClockSampler:
             v = sclk_mhz()
             if v is not None:
                 self.samples.append(v)
+            w = power_w()
+            if w is not None:
+                self.power.append(w)
             self._stop.wait(self.period)
 
     def __enter__(self):
@@ -98,6 +133,9 @@ class ClockSampler:
 
     def mean(self):
         return sum(self.samples) / len(self.samples) if self.samples else None
+
+    def mean_power(self):
+        return sum(self.power) / len(self.power) if self.power else None
 
 
 def memory_sweep():
@@ -516,6 +554,10 @@ def main():
                        "contraction)"),
         "sclk_mhz": round(clk, 1) if clk else None,
         "sclk_samples": len(clock.samples),
+        # board power during the timed region and the cap the driver enforces
+        # (the clock under this load is set by power)
+        "power_w": round(clock.mean_power(), 1) if clock.mean_power() else None,
+        "power_cap_w": power_cap_w(),
         "mfma_pct_at_measured_sclk": (round(100.0 * executed / (ms / 1e3)
                                             / (256 * 4096 * clk * 1e6), 2)
                                       if clk and w.dtype == "bf16" else None),
