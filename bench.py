@@ -555,7 +555,8 @@ def main():
         "sclk_mhz": round(clk, 1) if clk else None,
         "sclk_samples": len(clock.samples),
         # board power during the timed region and the cap the driver enforces
-        # (the clock under this load is set by power)
+        # (the clock under this load is set by power); the driver's reading
+        # trails the load, so it means something over a second or more
         "power_w": round(clock.mean_power(), 1) if clock.mean_power() else None,
         "power_cap_w": power_cap_w(),
         "mfma_pct_at_measured_sclk": (round(100.0 * executed / (ms / 1e3)
